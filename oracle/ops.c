@@ -1,0 +1,191 @@
+/*
+ * Oracle: the three operations of the hot path.
+ * TEST INFRASTRUCTURE ONLY (see oracle.h).
+ */
+#include "oracle.h"
+#include "oracle_internal.h"
+
+#include <math.h>
+#include <stddef.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+int orc_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ---- operand quantization ------------------------------------------------
+ * Sec. 2.1: weights, activations, errors and gradients are held in FP8 for
+ * all GEMMs.  The rounding into P8 is round-to-nearest-even (the paper names
+ * no mode for it).  An FP32 source is rounded once; a P16 source is first
+ * decoded exactly.  The value is multiplied by `scale` in FP32 first (used for
+ * loss scaling, Sec. 3). */
+int cpu_fp8_quantize(const void* src, int src_format, float scale,
+                     uint8_t* dst, int64_t n) {
+    if (n < 0) return ORC_EINVAL;
+    if (n > 0 && (!src || !dst)) return ORC_EINVAL;
+    if (src_format != ORC_SRC_F32 && src_format != ORC_SRC_P16) return ORC_EINVAL;
+    for (int64_t i = 0; i < n; i++) {
+        float x;
+        if (src_format == ORC_SRC_F32)
+            x = ((const float*)src)[i];
+        else
+            x = (float)orc_p16_value(((const uint16_t*)src)[i]);
+        volatile float xs = x * scale;          /* one FP32 product */
+        dst[i] = orc_q8((double)xs);
+    }
+    return ORC_OK;
+}
+
+/* ---- chunk-based reduced-precision dot products --------------------------
+ * Sec. 2.3, "Chunk-based Accumulation", and the dot-product algorithm of
+ * Fig. 3(a): the length-K dot product is cut into chunks of CL consecutive
+ * terms (starting at k = 0; the last chunk may be shorter).  Inside a chunk
+ * the products are added one by one, in ascending k, into one extra variable
+ * (the intra-chunk sum), rounding to P16 after every addition; after each
+ * chunk that partial sum is added, again with P16 rounding, into the running
+ * sum (inter-chunk accumulation).  Both sums start at +0.
+ *
+ * The fast mode (not in the paper) forms each chunk's partial sum exactly and
+ * rounds it to P16 once, then accumulates chunks exactly as above. */
+
+static inline uint8_t op_a(int trans_a, const uint8_t* A, int64_t lda,
+                           int64_t i, int64_t k) {
+    return trans_a ? A[k * lda + i] : A[i * lda + k];
+}
+
+static inline uint8_t op_b(int trans_b, const uint8_t* B, int64_t ldb,
+                           int64_t k, int64_t j) {
+    return trans_b ? B[j * ldb + k] : B[k * ldb + j];
+}
+
+static uint16_t chunk_dot(int trans_a, int trans_b, int64_t K, int64_t CL,
+                          const uint8_t* A, int64_t lda, const uint8_t* B,
+                          int64_t ldb, int mode, int64_t i, int64_t j) {
+    xnum S = xn_zero(0);
+    for (int64_t c0 = 0; c0 < K; c0 += CL) {
+        int64_t c1 = (K - c0 < CL) ? K : c0 + CL;
+        xnum P = xn_zero(0);
+        if (mode == ORC_EXACT) {
+            for (int64_t k = c0; k < c1; k++) {
+                xnum p = xn_mul_p8(op_a(trans_a, A, lda, i, k),
+                                   op_b(trans_b, B, ldb, k, j));
+                P = xn_from_p16(xn_round_p16(xn_add(P, p)));
+            }
+        } else {
+            xnum sum = xn_zero(0);
+            for (int64_t k = c0; k < c1; k++) {
+                xnum p = xn_mul_p8(op_a(trans_a, A, lda, i, k),
+                                   op_b(trans_b, B, ldb, k, j));
+                sum = xn_add(sum, p);
+            }
+            P = xn_from_p16(xn_round_p16(xn_add(P, sum)));
+        }
+        S = xn_from_p16(xn_round_p16(xn_add(S, P)));
+    }
+    return xn_round_p16(S);
+}
+
+static int gemm_args_ok(int trans_a, int trans_b, int64_t M, int64_t N,
+                        int64_t K, int64_t CL, const uint8_t* A, int64_t lda,
+                        const uint8_t* B, int64_t ldb, int mode) {
+    if (M < 0 || N < 0 || K < 0 || CL < 1) return 0;
+    if ((trans_a != 0 && trans_a != 1) || (trans_b != 0 && trans_b != 1)) return 0;
+    if (mode != ORC_EXACT && mode != ORC_FAST) return 0;
+    if (M > 0 && N > 0 && K > 0) {
+        if (!A || !B) return 0;
+        if (lda < (trans_a ? M : K)) return 0;
+        if (ldb < (trans_b ? K : N)) return 0;
+    }
+    return 1;
+}
+
+int cpu_chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                   int64_t CL, const uint8_t* A, int64_t lda,
+                   const uint8_t* B, int64_t ldb, uint16_t* C, int64_t ldc,
+                   int mode) {
+    if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, mode))
+        return ORC_EINVAL;
+    if (M > 0 && N > 0 && (!C || ldc < N)) return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; i++)
+        for (int64_t j = 0; j < N; j++)
+            C[i * ldc + j] = chunk_dot(trans_a, trans_b, K, CL, A, lda, B, ldb,
+                                       mode, i, j);
+    return ORC_OK;
+}
+
+int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
+                          int64_t K, int64_t CL, const uint8_t* A, int64_t lda,
+                          const uint8_t* B, int64_t ldb, int mode,
+                          const int64_t* rows, const int64_t* cols,
+                          int64_t npts, uint16_t* out) {
+    if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, mode))
+        return ORC_EINVAL;
+    if (npts < 0 || (npts > 0 && (!rows || !cols || !out))) return ORC_EINVAL;
+    for (int64_t p = 0; p < npts; p++)
+        if (rows[p] < 0 || rows[p] >= M || cols[p] < 0 || cols[p] >= N)
+            return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t p = 0; p < npts; p++)
+        out[p] = chunk_dot(trans_a, trans_b, K, CL, A, lda, B, ldb, mode,
+                           rows[p], cols[p]);
+    return ORC_OK;
+}
+
+/* ---- SGD weight update in P16 with stochastic rounding -------------------
+ * Sec. 2.2 (Fig. 2(b)) and Sec. 4.3: the three AXPYs of an SGD step --
+ * L2 regularisation, momentum accumulation and the weight update -- all run
+ * in P16 with floating-point stochastic rounding (Eq. (1)); Sec. 3 keeps a
+ * P16 master copy and an FP8 copy of the weights.  Each AXPY is one FP32
+ * fused multiply-add followed by one stochastic rounding into P16:
+ *     g' = SR16(wd * w + g)
+ *     v' = SR16(momentum * v + g')       (skipped when v is absent)
+ *     w' = SR16(-lr * v' + w)            (-lr * g' + w when v is absent)
+ *     w8 = Q8(w')
+ * Random bits: one Philox4x32-10 block per element pair, key = seed,
+ * counter = (pair index, offset), each 32-bit word split into two 16-bit
+ * uniforms (low half first); element i takes uniforms 3*(i mod 2) + 0, 1, 2
+ * for the three roundings in the order above. */
+int cpu_sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v,
+                         uint8_t* w8, int64_t n, float lr, float momentum,
+                         float weight_decay, uint64_t seed, uint64_t offset) {
+    if (n < 0) return ORC_EINVAL;
+    if (n > 0 && (!w || !g)) return ORC_EINVAL;
+    if (momentum != 0.0f && !v) return ORC_EINVAL;
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++) {
+        uint64_t pair = (uint64_t)i >> 1;
+        const uint32_t ctr[4] = {(uint32_t)pair, (uint32_t)(pair >> 32),
+                                 (uint32_t)offset, (uint32_t)(offset >> 32)};
+        uint32_t words[4];
+        orc_philox4x32_10(ctr, key, words);
+        uint32_t u[8];
+        for (int q = 0; q < 4; q++) {
+            u[2 * q] = words[q] & 0xFFFFu;
+            u[2 * q + 1] = words[q] >> 16;
+        }
+        const uint32_t* h = u + 3 * (i & 1);
+
+        float wf = (float)orc_p16_value(w[i]);
+        float gf = (float)orc_p16_value(g[i]);
+        uint16_t g1 = orc_sr16(fmaf(weight_decay, wf, gf), h[0]);
+        float step = (float)orc_p16_value(g1);
+        if (v) {
+            float vf = (float)orc_p16_value(v[i]);
+            uint16_t v1 = orc_sr16(fmaf(momentum, vf, step), h[1]);
+            v[i] = v1;
+            step = (float)orc_p16_value(v1);
+        }
+        uint16_t w1 = orc_sr16(fmaf(-lr, step, wf), h[2]);
+        w[i] = w1;
+        if (w8) w8[i] = orc_q8(orc_p16_value(w1));
+    }
+    return ORC_OK;
+}
