@@ -1,0 +1,231 @@
+"""Benchmark of the FP8-training hot path on one MI355X.
+
+One step = one training pass of a 3x3 convolution stage of a 50-layer
+residual CNN (batch 256, 14x14, 256 -> 256 channels) lowered to GEMMs:
+
+  1. fp8_quantize the lowered activations (50176 x 2304) and the loss-scaled
+     errors (50176 x 256, scale 1024) from FP32;
+  2. chunk_gemm, exact mode, CL = 64: Forward Y = X W (50176x256x2304),
+     Backward dX = dY W^T (50176x2304x256), Gradient dW = X^T dY
+     (2304x256x50176);
+  3. the same three GEMMs in fast mode (FP8 matrix cores within a chunk);
+  4. sr_weight_update of the 2304 x 256 FP16 master weights with the exact
+     Gradient GEMM's FP16 output, momentum 0.9, weight decay 1e-4, writing
+     the FP8 weight copy used by the next step's GEMMs.
+
+Inputs are seeded synthetic data (workloads.conv_gemms), resident in HBM
+before timing.  `value` = all chunk_gemm multiply-accumulates of a step
+(3 exact + 3 fast GEMMs) / step time, in GMAC/s.  Per-kernel times come from
+HIP events recorded on the stream the library launches on.
+
+    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+CL = 64
+METRIC = "chunk_gemm GMAC/s (exact & fast mode) + % VALU/MFMA peak; SR update GB/s"
+
+# MI355X published figures
+CUS, CLOCK_HZ, LANES = 256, 2.4e9, 64
+VALU_LANE_OPS = CUS * LANES * CLOCK_HZ                  # 39.3e12 32-bit lane-ops/s
+HBM_BYTES_S = 8.0e12
+FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
+
+
+def exact_peak_mac_s(cl):
+    """Emulation ceiling of one exact-mode multiply-accumulate: gfx950 has no
+    adder for the paper's FP16, so a MAC costs at least one FP32 FMA plus
+    three integer ops that round the result to a 10-bit significand, and each
+    chunk end adds one more add + rounding (4 ops) per output."""
+    return VALU_LANE_OPS / (4.0 + 4.0 / cl)
+
+
+def fast_peak_mac_s(cl):
+    """Fast mode: min(FP8 MFMA peak, VALU epilogue of 8 ops per output per
+    chunk: scale, round, add, round)."""
+    return min(FP8_MFMA_MAC_S, VALU_LANE_OPS * cl / 8.0)
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0,
+                   help="target wall time of the oracle sample")
+    return p.parse_args()
+
+
+def cpu_baseline(work, target_s):
+    """The oracle, as it stands, on a bounded sample of the same workload:
+    exact-mode outputs of the three GEMMs at sampled positions."""
+    import oracle
+    Xo = oracle.fp8_quantize(work["Xcol"])
+    Wo = oracle.fp8_quantize(work["W"])
+    Do = oracle.fp8_quantize(work["dY"], work["dy_scale"])
+    M, K = work["Xcol"].shape
+    N = work["W"].shape[1]
+    gemms = [("fwd", Xo, Wo, M, N, K, 0, 0), ("dgrad", Do, Wo, M, K, N, 0, 1),
+             ("wgrad", Xo, Do, K, N, M, 1, 0)]
+    rng = np.random.default_rng(99)
+
+    def run(npts):
+        macs, t = 0, 0.0
+        for _, A, B, m, n, k, ta, tb in gemms:
+            r = rng.integers(0, m, npts)
+            c = rng.integers(0, n, npts)
+            t0 = time.perf_counter()
+            oracle.chunk_gemm_points(A, B, CL, r, c, ta, tb)
+            t += time.perf_counter() - t0
+            macs += npts * k
+        return macs, t
+
+    macs, t = run(16)                                     # calibrate
+    npts = int(max(16, min(20000, 16 * target_s / max(t, 1e-3))))
+    macs, t = run(npts)
+    return {"value": macs / t / 1e9, "unit": "GMAC/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"exact mode, CL {CL}: {npts} sampled outputs of each of the forward, "
+                      f"backward and gradient GEMMs ({macs / 1e6:.0f} M MAC, {t:.1f} s)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the path is "
+              "single-GPU by design", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_1812_08011_amd as fp8t
+    import workloads
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    fp8t.lib()
+    work = workloads.conv_gemms()
+    X32 = torch.from_numpy(work["Xcol"]).to(dev)
+    W32 = torch.from_numpy(work["W"]).to(dev)
+    D32 = torch.from_numpy(work["dY"]).to(dev)
+    M, K = X32.shape
+    N = W32.shape[1]
+    u8 = lambda *s: torch.empty(*s, dtype=torch.uint8, device=dev)
+    u16 = lambda *s: torch.empty(*s, dtype=torch.uint16, device=dev)
+    X8, D8 = u8(M, K), u8(M, N)
+    W16, V16, W8 = u16(K, N), u16(K, N), u8(K, N)
+    fp8t.fp16_quantize(W32, W16)
+    fp8t.fp16_quantize(torch.zeros_like(W32), V16)
+    fp8t.fp8_quantize(W16, W8)
+    outs = {m: (u16(M, N), u16(M, K), u16(K, N)) for m in (fp8t.EXACT, fp8t.FAST)}
+    n_w = K * N
+    gemm_macs = M * N * K
+
+    names = ["quantize", "exact_fwd", "exact_dgrad", "exact_wgrad", "fast_fwd", "fast_dgrad",
+             "fast_wgrad", "sr_update"]
+
+    def step(i, ev=None):
+        def mark(j):
+            if ev is not None:
+                ev[j].record()
+        mark(0)
+        fp8t.fp8_quantize(X32, X8)
+        fp8t.fp8_quantize(D32, D8, work["dy_scale"])
+        mark(1)
+        j = 1
+        for mode in (fp8t.EXACT, fp8t.FAST):
+            Y, dX, dW = outs[mode]
+            fp8t.chunk_gemm(0, 0, M, N, K, CL, X8, K, W8, N, Y, N, mode)
+            j += 1; mark(j)
+            fp8t.chunk_gemm(0, 1, M, K, N, CL, D8, N, W8, N, dX, K, mode)
+            j += 1; mark(j)
+            fp8t.chunk_gemm(1, 0, K, N, M, CL, X8, K, D8, N, dW, N, mode)
+            j += 1; mark(j)
+        fp8t.sr_weight_update(W16, outs[fp8t.EXACT][2], V16, W8, n_w, 0.1, 0.9, 1e-4,
+                              7, i)
+        mark(8)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(args.warmup + s, evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = {k: 0.0 for k in names}
+    for s in range(args.steps):
+        for j, k in enumerate(names):
+            per[k] += evs[s][j].elapsed_time(evs[s][j + 1]) / 1e3
+    per = {k: v / args.steps for k, v in per.items()}       # seconds per step
+
+    step_s = wall / args.steps
+    total_macs = 6 * gemm_macs
+    exact_s = per["exact_fwd"] + per["exact_dgrad"] + per["exact_wgrad"]
+    fast_s = per["fast_fwd"] + per["fast_dgrad"] + per["fast_wgrad"]
+    upd_bytes = 11 * n_w
+    q_bytes = 5 * (M * K + M * N)
+    exact_avg = exact_s / 3
+    exact_achieved = gemm_macs / exact_avg
+    peak = exact_peak_mac_s(CL)
+
+    result = {
+        "metric": METRIC,
+        "value": total_macs / step_s / 1e9,
+        "unit": "GMAC/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8(1,5,2) products, fp16(1,6,9) accumulation (emulated in f32+int)",
+        "data": "synthetic",
+        "config": {
+            "workload": "resnet50-like 3x3 conv stage lowered to GEMMs: batch 256, 14x14, "
+                        "256->256 ch; fwd 50176x256x2304, dgrad 50176x2304x256, wgrad "
+                        "2304x256x50176; CL 64; exact + fast; SR update of 2304x256 weights",
+            "global_batch": 256,
+            "chunk_len": CL,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "kernel": "chunk_gemm exact",
+            "bound": "alu",
+            "achieved": exact_achieved / 1e12,
+            "peak": peak / 1e12,
+            "unit": "TMAC/s",
+            "frac": exact_achieved / peak,
+            "traffic": None,
+        },
+        "kernels": {
+            "exact_gemm_gmac_s": 3 * gemm_macs / exact_s / 1e9,
+            "exact_frac_of_valu_emulation_peak": 3 * gemm_macs / exact_s / peak,
+            "exact_ms": {k: per[k] * 1e3 for k in ("exact_fwd", "exact_dgrad", "exact_wgrad")},
+            "fast_gemm_gmac_s": 3 * gemm_macs / fast_s / 1e9,
+            "fast_frac_of_fp8_mfma_peak": 3 * gemm_macs / fast_s / FP8_MFMA_MAC_S,
+            "fast_frac_of_fast_bound": 3 * gemm_macs / fast_s / fast_peak_mac_s(CL),
+            "fast_ms": {k: per[k] * 1e3 for k in ("fast_fwd", "fast_dgrad", "fast_wgrad")},
+            "sr_update_gb_s": upd_bytes / per["sr_update"] / 1e9,
+            "sr_update_us": per["sr_update"] * 1e6,
+            "quantize_gb_s": q_bytes / per["quantize"] / 1e9,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(work, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,164 @@
+/*
+ * fp8train -- the hot path of 8-bit floating-point training (Wang, Choi,
+ * Brand, Chen, Gopalakrishnan, "Training Deep Neural Networks with 8-bit
+ * Floating Point Numbers", NeurIPS 2018) for AMD MI355X (gfx950).
+ *
+ * Number formats (Sec. 2.2), stored as raw codes:
+ *   FP8  (1 sign, 5 exponent, 2 mantissa bits) in uint8_t,  bias 15.
+ *   FP16 (1 sign, 6 exponent, 9 mantissa bits) in uint16_t, bias 31.
+ *        This FP16 is the paper's format, NOT IEEE binary16.
+ * Both have gradual underflow; the all-ones exponent field holds Inf
+ * (mantissa 0) and NaN.  FP8 quantization saturates finite overflow at
+ * +-57344; FP16 results beyond +-(2 - 2^-9) * 2^31 become +-Inf.  Every NaN
+ * result is written as the canonical code 0x7F (FP8) or 0x7F00 (FP16).
+ * Rounding to nearest breaks ties to even.
+ *
+ * Conventions for every call:
+ *   - All array pointers are device pointers owned by the caller.  The
+ *     library never allocates, frees or synchronizes; work is enqueued on
+ *     `stream` (0 = the null stream) and runs asynchronously.
+ *   - Arguments are validated before anything is enqueued.  A call that
+ *     returns an error has enqueued nothing.
+ *   - Sizes are element counts.  Matrices are row-major with a leading
+ *     dimension (elements between consecutive rows).
+ *   - Outputs must not alias inputs unless stated.
+ */
+#ifndef FP8TRAIN_H
+#define FP8TRAIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+    FP8T_OK = 0,
+    FP8T_EINVAL = -1,     /* invalid argument; nothing was enqueued          */
+    FP8T_EWORKSPACE = -2, /* workspace smaller than chunk_gemm_workspace_size */
+    FP8T_EHIP = -3        /* the HIP runtime reported an error at launch     */
+};
+
+/* Source formats for fp8_quantize. */
+enum { FP8T_SRC_F32 = 0, FP8T_SRC_FP16 = 1 };
+
+/* chunk_gemm modes. */
+enum { FP8T_EXACT = 0, FP8T_FAST = 1 };
+
+/*
+ * fp8_quantize -- round values into FP8 (Sec. 2.1: weights, activations,
+ * errors and gradients enter every GEMM as 8-bit floats).
+ *
+ *   dst[i] = Q8(RN32(x[i] * scale))
+ *
+ * x[i] is src[i] as an IEEE float (src_format FP8T_SRC_F32, `src` points to
+ * float) or the exact value of the FP16 code src[i] (FP8T_SRC_FP16, `src`
+ * points to uint16_t).  The product with `scale` (e.g. a loss scale, Sec. 3)
+ * is one IEEE single-precision multiplication; Q8 rounds it to the nearest FP8
+ * value, ties to even, with gradual underflow below 2^-14 and saturation at
+ * +-57344.  n >= 0 elements; src and dst contiguous; n == 0 is a no-op.
+ * Errors: FP8T_EINVAL for n < 0, a NULL pointer with n > 0, or an unknown
+ * src_format.
+ */
+int fp8_quantize(const void* src, int src_format, float scale, uint8_t* dst,
+                 int64_t n, hipStream_t stream);
+
+/*
+ * fp16_quantize -- round IEEE floats to the nearest FP16 (1,6,9) value, ties
+ * to even (the round-to-nearest of Sec. 2.2), e.g. to create the FP16 master
+ * copy of the weights (Sec. 3).  Overflow gives +-Inf.  n >= 0, contiguous.
+ * Errors: FP8T_EINVAL for n < 0 or a NULL pointer with n > 0.
+ */
+int fp16_quantize(const float* src, uint16_t* dst, int64_t n,
+                  hipStream_t stream);
+
+/*
+ * chunk_gemm -- C = op(A) * op(B) with FP8 operands and chunk-based FP16
+ * accumulation (Sec. 2.3 "Chunk-based Accumulation" and the dot-product
+ * algorithm of Fig. 3(a)); used for the Forward, Backward and Gradient GEMMs
+ * of Sec. 2.2 through the transpose flags.
+ *
+ * For every output (i, j), with a(k) = op(A)(i, k), b(k) = op(B)(k, j):
+ *   the K products a(k) * b(k) (exact) are split into chunks of CL
+ *   consecutive k starting at k = 0 (the last chunk may be shorter);
+ *   mode FP8T_EXACT: within a chunk, products are added in ascending k into
+ *     an intra-chunk sum starting at +0, rounding to FP16 after every add;
+ *   mode FP8T_FAST:  a chunk's products are summed in FP32 on the matrix
+ *     cores (in an unspecified order), and the sum is rounded to FP16 once;
+ *   each chunk's sum is then added, in ascending chunk order, into the
+ *     running sum starting at +0, rounding to FP16 after every add;
+ *   C(i, j) = the FP16 code of the running sum (+0 when K == 0).
+ * FP8T_EXACT is bit-exact.  FP8T_FAST differs only in the rounding inside a
+ * chunk.  With CL not a multiple of 16 the fast mode sums a chunk
+ * sequentially in FP32 on the vector ALUs instead; the semantics are the same.
+ *
+ * Layouts (row-major):
+ *   op(A) is M x K: A is stored M x K (trans_a = 0, lda >= K) or
+ *                   K x M (trans_a = 1, lda >= M), op(A) = A^T.
+ *   op(B) is K x N: B is stored K x N (trans_b = 0, ldb >= N) or
+ *                   N x K (trans_b = 1, ldb >= K), op(B) = B^T.
+ *   C is M x N with ldc >= N.
+ * Forward Y = X W: (0, 0).  Backward dX = dY W^T: trans_b = 1.
+ * Gradient dW = X^T dY: trans_a = 1.
+ * M, N, K >= 0; CL >= 1 (CL >= K means one chunk).  C must not overlap A or B.
+ * workspace / workspace_bytes: device scratch of at least
+ * chunk_gemm_workspace_size(...) bytes for the same arguments (may be NULL
+ * when that size is 0); its contents on entry do not matter.
+ * Errors: FP8T_EINVAL (negative size, CL < 1, flag not 0/1, a leading
+ * dimension too small, NULL pointer for a non-empty matrix);
+ * FP8T_EWORKSPACE; FP8T_EHIP.
+ */
+int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+               int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+               int64_t ldb, uint16_t* C, int64_t ldc, int mode,
+               void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * chunk_gemm_workspace_size -- bytes of workspace chunk_gemm needs for these
+ * arguments (0 if none).  Returns 0 for invalid arguments as well.
+ */
+size_t chunk_gemm_workspace_size(int trans_a, int trans_b, int64_t M,
+                                 int64_t N, int64_t K, int64_t CL, int mode);
+
+/*
+ * sr_weight_update -- one SGD step entirely in FP16 with floating-point
+ * stochastic rounding (Sec. 2.2 / Fig. 2(b): L2-Reg, Momentum-Acc and
+ * Weight-Upd AXPYs; Sec. 2.3 Eq. (1); Sec. 4.3), keeping the FP16 master
+ * weights and writing the FP8 copy used by the next step's GEMMs (Sec. 3).
+ *
+ * For i in [0, n), with SR(.) = stochastic rounding into FP16 of an IEEE
+ * float (Eq. (1) with k = 9 of k' = 23 mantissa bits: the magnitude is rounded
+ * up by one FP16 step with probability equal to the discarded fraction of a
+ * step, using a 16-bit uniform; below 2^-30 the step is 2^-39):
+ *   g' = SR(fmaf(weight_decay, w[i], g[i]))
+ *   v' = SR(fmaf(momentum, v[i], g'))          (only if v != NULL)
+ *   w' = SR(fmaf(-lr, v', w[i]))               (-lr * g' if v == NULL)
+ *   w[i] = w', v[i] = v', w8[i] = FP8 of w' (round to nearest even, saturating)
+ * fmaf is the IEEE single-precision fused multiply-add.  The uniforms: one
+ * Philox4x32-10 block (Salmon et al., SC'11) per element pair with key =
+ * (seed low, seed high) and counter = (i/2 low, i/2 high, offset low, offset
+ * high); its four 32-bit words give eight 16-bit uniforms (low half first) and
+ * element i uses uniforms 3*(i%2)+0, +1, +2 for g', v', w'.  The result is a
+ * pure function of (w, g, v, n, lr, momentum, weight_decay, seed, offset).
+ *
+ * w, g: FP16 codes [n]; w is updated in place.  v: FP16 momentum buffer [n],
+ * updated in place, or NULL (then momentum must be 0).  w8: FP8 codes [n] or
+ * NULL (no copy).  w8 must not overlap w.
+ * Errors: FP8T_EINVAL (n < 0, NULL w or g with n > 0, v == NULL with
+ * momentum != 0); FP8T_EHIP.
+ */
+int sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v, uint8_t* w8,
+                     int64_t n, float lr, float momentum, float weight_decay,
+                     uint64_t seed, uint64_t offset, hipStream_t stream);
+
+/* A static, human-readable description of a status code. */
+const char* fp8t_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

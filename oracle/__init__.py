@@ -59,6 +59,8 @@ def lib():
         L.orc_philox4x32_10.argtypes = [vp, vp, vp]
         L.cpu_fp8_quantize.restype = ctypes.c_int
         L.cpu_fp8_quantize.argtypes = [vp, ctypes.c_int, f32, vp, i64]
+        L.cpu_fp16_quantize.restype = ctypes.c_int
+        L.cpu_fp16_quantize.argtypes = [vp, vp, i64]
         L.cpu_chunk_gemm.restype = ctypes.c_int
         L.cpu_chunk_gemm.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64, i64,
                                      vp, i64, vp, i64, vp, i64, ctypes.c_int]
@@ -149,6 +151,14 @@ def fp8_quantize(src, scale=1.0):
     dst = np.empty(src.shape, dtype=np.uint8)
     _check(lib().cpu_fp8_quantize(_ptr(src), fmt, float(scale), _ptr(dst), src.size),
            "fp8_quantize")
+    return dst
+
+
+def fp16_quantize(src):
+    """float32 array -> P16 codes (uint16), round to nearest even."""
+    src = np.ascontiguousarray(src, dtype=np.float32)
+    dst = np.empty(src.shape, dtype=np.uint16)
+    _check(lib().cpu_fp16_quantize(_ptr(src), _ptr(dst), src.size), "fp16_quantize")
     return dst
 
 

@@ -199,11 +199,25 @@ uint8_t orc_q8(double x) {
     return (uint8_t)(s | ((e + 15) << 2) | ((int)n - 4));
 }
 
+/* RN16: round any double to the nearest P16 value, ties to even, gradual
+ * underflow below 2^-30 with step 2^-39, overflow to +-Inf. */
 uint16_t orc_rn16(double x) {
-    /* x must be a multiple of 2^-39 below 2^89 (any double that is a P8
-     * value, a P16 value, an FP32 value of magnitude >= 2^-16 ... ); the
-     * general case goes through the exact integer path. */
-    return xn_round_p16(xn_from_double(x));
+    if (isnan(x)) return 0x7F00u;
+    uint16_t s = (uint16_t)(signbit(x) ? 0x8000u : 0u);
+    if (isinf(x)) return (uint16_t)(s | 0x7E00u);
+    double a = fabs(x);
+    if (a < ldexp(1.0, -30)) {
+        double n = rne_int(ldexp(a, 39));   /* 0..512; 512 is 2^-30 = 0x0200 */
+        return (uint16_t)(s | (uint16_t)n);
+    }
+    int E;
+    (void)frexp(a, &E);
+    int e = E - 1;                          /* a in [2^e, 2^(e+1))          */
+    if (e > 31) return (uint16_t)(s | 0x7E00u);
+    double n = rne_int(ldexp(a, 9 - e));    /* significand * 512, [512,1024] */
+    if (n == 1024.0) { n = 512.0; e++; }
+    if (e > 31) return (uint16_t)(s | 0x7E00u);
+    return (uint16_t)(s | ((e + 31) << 9) | ((int)n - 512));
 }
 
 uint16_t orc_add16(uint16_t x, uint16_t y) {

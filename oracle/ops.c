@@ -42,6 +42,15 @@ int cpu_fp8_quantize(const void* src, int src_format, float scale,
     return ORC_OK;
 }
 
+/* Round FP32 values to the nearest P16 value, ties to even (Sec. 2.2 names
+ * round-to-nearest for P16; used to create P16 master weights, Sec. 3). */
+int cpu_fp16_quantize(const float* src, uint16_t* dst, int64_t n) {
+    if (n < 0) return ORC_EINVAL;
+    if (n > 0 && (!src || !dst)) return ORC_EINVAL;
+    for (int64_t i = 0; i < n; i++) dst[i] = orc_rn16((double)src[i]);
+    return ORC_OK;
+}
+
 /* ---- chunk-based reduced-precision dot products --------------------------
  * Sec. 2.3, "Chunk-based Accumulation", and the dot-product algorithm of
  * Fig. 3(a): the length-K dot product is cut into chunks of CL consecutive

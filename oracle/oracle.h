@@ -50,6 +50,9 @@ void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2],
 int cpu_fp8_quantize(const void* src, int src_format, float scale,
                      uint8_t* dst, int64_t n);
 
+/* FP32 -> P16, round to nearest even (creates P16 master copies). */
+int cpu_fp16_quantize(const float* src, uint16_t* dst, int64_t n);
+
 int cpu_chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                    int64_t CL, const uint8_t* A, int64_t lda,
                    const uint8_t* B, int64_t ldb, uint16_t* C, int64_t ldc,

@@ -1,0 +1,135 @@
+"""Python binding of libfp8train (include/fp8train.h).
+
+Argument marshalling only: every step runs in the HIP library.  Arrays are
+torch tensors on the GPU (uint8 for FP8 codes, uint16 for FP16 codes, float32
+for IEEE inputs); work goes onto torch's current HIP stream unless a stream is
+given.  A call that the library rejects raises Fp8tError.  There is no CPU
+fallback: if the library is not built, every call raises.
+"""
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libfp8train.so")
+
+OK, EINVAL, EWORKSPACE, EHIP = 0, -1, -2, -3
+SRC_F32, SRC_FP16 = 0, 1
+EXACT, FAST = 0, 1
+
+_lib = None
+
+
+class Fp8tError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__(f"{fn}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+def lib():
+    """The loaded library.  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is not built; run `python -m paper_1812_08011_amd.build` "
+                "or __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        i32, i64, u64, f32, vp, sz = (ctypes.c_int, ctypes.c_int64, ctypes.c_uint64,
+                                      ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t)
+        L.fp8_quantize.restype = i32
+        L.fp8_quantize.argtypes = [vp, i32, f32, vp, i64, vp]
+        L.fp16_quantize.restype = i32
+        L.fp16_quantize.argtypes = [vp, vp, i64, vp]
+        L.chunk_gemm.restype = i32
+        L.chunk_gemm.argtypes = [i32, i32, i64, i64, i64, i64, vp, i64, vp, i64, vp, i64,
+                                 i32, vp, sz, vp]
+        L.chunk_gemm_workspace_size.restype = sz
+        L.chunk_gemm_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64, i32]
+        L.sr_weight_update.restype = i32
+        L.sr_weight_update.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, u64, u64, vp]
+        L.fp8t_status_string.restype = ctypes.c_char_p
+        L.fp8t_status_string.argtypes = [i32]
+        _lib = L
+    return _lib
+
+
+def status_string(status):
+    return lib().fp8t_status_string(int(status)).decode()
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(fn, status):
+    if status != OK:
+        raise Fp8tError(fn, status)
+
+
+def fp8_quantize(src, dst, scale=1.0, stream=None):
+    """dst (uint8, FP8 codes) = Q8(src * scale); src float32 or uint16 FP16 codes."""
+    import torch
+    if src.dtype == torch.float32:
+        fmt = SRC_F32
+    elif src.dtype == torch.uint16:
+        fmt = SRC_FP16
+    else:
+        raise TypeError("fp8_quantize: src must be float32 or uint16 (FP16 codes)")
+    if dst.dtype != torch.uint8 or dst.numel() != src.numel():
+        raise TypeError("fp8_quantize: dst must be uint8 with as many elements as src")
+    if not (src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("fp8_quantize: tensors must be contiguous")
+    _check("fp8_quantize", lib().fp8_quantize(_ptr(src), fmt, float(scale), _ptr(dst),
+                                               src.numel(), _stream(stream)))
+    return dst
+
+
+def fp16_quantize(src, dst, stream=None):
+    """dst (uint16, FP16 codes) = round-to-nearest-even of float32 src."""
+    import torch
+    if src.dtype != torch.float32 or dst.dtype != torch.uint16 or dst.numel() != src.numel():
+        raise TypeError("fp16_quantize: float32 src, uint16 dst of the same size")
+    if not (src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("fp16_quantize: tensors must be contiguous")
+    _check("fp16_quantize", lib().fp16_quantize(_ptr(src), _ptr(dst), src.numel(),
+                                                 _stream(stream)))
+    return dst
+
+
+def chunk_gemm_workspace_size(trans_a, trans_b, M, N, K, CL, mode):
+    return int(lib().chunk_gemm_workspace_size(int(trans_a), int(trans_b), int(M), int(N),
+                                               int(K), int(CL), int(mode)))
+
+
+def chunk_gemm(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, mode=EXACT,
+               workspace=None, workspace_bytes=0, stream=None):
+    """The C-ABI call with the same argument order; A, B, C, workspace are
+    tensors (or raw device addresses)."""
+    _check("chunk_gemm", lib().chunk_gemm(int(trans_a), int(trans_b), int(M), int(N), int(K),
+                                          int(CL), _ptr(A), int(lda), _ptr(B), int(ldb),
+                                          _ptr(C), int(ldc), int(mode), _ptr(workspace),
+                                          int(workspace_bytes), _stream(stream)))
+    return C
+
+
+def sr_weight_update(w, g, v, w8, n, lr, momentum, weight_decay, seed, offset, stream=None):
+    """The C-ABI call with the same argument order; w, g, v, w8 are tensors
+    (v, w8 may be None)."""
+    _check("sr_weight_update",
+           lib().sr_weight_update(_ptr(w), _ptr(g), _ptr(v), _ptr(w8), int(n), float(lr),
+                                  float(momentum), float(weight_decay), int(seed), int(offset),
+                                  _stream(stream)))
+    return w

@@ -1,0 +1,174 @@
+// Device-side number-format helpers for gfx950.
+//
+// FP8 = (1,5,2) bias 15 and FP16 = (1,6,9) bias 31 (Sec. 2.2), both with
+// gradual underflow; the all-ones exponent holds Inf/NaN.
+//
+// The GEMM kernels work in a *scaled FP32 domain*: every FP16 quantity x is
+// held as the IEEE float x * 2^96.  In that domain
+//   - every FP16 value (2^-39 .. 2^32) maps to a normal float (2^57 .. 2^128),
+//     so FP32 denormals never occur;
+//   - the FP16 overflow threshold 2^32 maps onto FP32's own 2^128, so the
+//     carry out of rounding the largest values lands exactly on the FP32 Inf
+//     encoding and FP16 overflow needs no extra instruction.
+// Rounding to FP16 is then "round the FP32 significand to 10 bits, ties to
+// even" on the raw bits.  FP32 addition first rounds the exact sum to 24 bits;
+// because 24 >= 2*10 + 1 that double rounding is innocuous (Figueroa 1995),
+// and below 2^-30 (FP16 subnormals) sums of FP16 values are exact in FP32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fp8t {
+
+constexpr uint32_t kF32Inf = 0x7F800000u;
+constexpr uint32_t kF32NaN = 0x7FC00000u;
+constexpr uint16_t kFp16NaN = 0x7F00u;
+constexpr uint16_t kFp16Inf = 0x7E00u;
+constexpr uint32_t kFp8NaN = 0x7Fu;
+
+// Round a scaled-domain float to the FP16 grid: keep 9 of the 23 stored
+// mantissa bits, ties to even (bfe + add3 + and).
+__device__ __forceinline__ float rn16s(float x) {
+    uint32_t u = __float_as_uint(x);
+    u = (u + 0x1FFFu + ((u >> 14) & 1u)) & 0xFFFFC000u;
+    return __uint_as_float(u);
+}
+
+// FP8 code -> float times 2^SHIFT (exact).  SHIFT = 96 gives the scaled
+// domain for one GEMM operand, 0 the plain value.
+template <int SHIFT>
+__device__ __forceinline__ float fp8_to_f32(uint32_t c) {
+    uint32_t mag = c & 0x7Fu;
+    uint32_t bits;
+    if (mag >= 0x7Cu) {
+        bits = (mag == 0x7Cu) ? kF32Inf : kF32NaN;
+    } else if (mag >= 4u) {
+        // normal: exponent field e (1..30), value (1 + m/4) 2^(e-15)
+        bits = (mag << 21) + ((uint32_t)(112 + SHIFT) << 23);
+    } else {
+        // subnormal: m * 2^-16
+        bits = __float_as_uint((float)mag * __builtin_ldexpf(1.0f, SHIFT - 16));
+    }
+    return __uint_as_float(bits | ((c & 0x80u) << 24));
+}
+
+// FP16 code -> plain float (exact; every FP16 value is an FP32 value).
+__device__ __forceinline__ float fp16_to_f32(uint32_t c) {
+    uint32_t e = (c >> 9) & 63u, m = c & 511u;
+    uint32_t bits;
+    if (e == 63u) {
+        bits = m ? kF32NaN : kF32Inf;
+    } else if (e == 0u) {
+        bits = __float_as_uint((float)m * 0x1p-39f);
+    } else {
+        bits = ((c & 0x7FFFu) << 14) + (96u << 23);
+    }
+    return __uint_as_float(bits | ((c & 0x8000u) << 16));
+}
+
+// Scaled-domain float already on the FP16 grid (low 14 bits zero) -> code.
+__device__ __forceinline__ uint16_t f32s_to_fp16(float x) {
+    uint32_t u = __float_as_uint(x);
+    uint32_t s = (u >> 16) & 0x8000u;
+    uint32_t a = u & 0x7FFFFFFFu;
+    if (a > kF32Inf) return kFp16NaN;
+    if (a >= (193u << 23))                       // >= 2^-30 (scaled 2^66)
+        return (uint16_t)(s | ((a >> 14) - (192u << 9)));
+    uint32_t k = (uint32_t)(__uint_as_float(a) * 0x1p-57f);   // subnormal
+    return (uint16_t)(s | k);
+}
+
+// Plain float -> nearest FP16 code, ties to even; overflow -> Inf.
+__device__ __forceinline__ uint16_t f32_to_fp16_rn(float x) {
+    uint32_t u = __float_as_uint(x);
+    uint32_t s = (u >> 16) & 0x8000u;
+    uint32_t a = u & 0x7FFFFFFFu;
+    if (a > kF32Inf) return kFp16NaN;
+    if (a >= (97u << 23)) {                      // >= 2^-30: normal range
+        uint32_t b = (a + 0x1FFFu + ((a >> 14) & 1u)) & 0xFFFFC000u;
+        if (b >= (159u << 23)) return (uint16_t)(s | kFp16Inf);   // >= 2^32
+        return (uint16_t)(s | ((b >> 14) - (96u << 9)));
+    }
+    // below 2^-30 the step is 2^-39: round |x| * 2^39 to an integer (<= 512)
+    float t = __builtin_rintf(__uint_as_float(a) * 0x1p39f);
+    return (uint16_t)(s | (uint32_t)t);
+}
+
+// Plain float -> nearest FP8 code, ties to even, gradual underflow below
+// 2^-14, finite overflow saturating at 57344.
+__device__ __forceinline__ uint32_t f32_to_fp8(float x) {
+    uint32_t u = __float_as_uint(x);
+    uint32_t s = (u >> 24) & 0x80u;
+    uint32_t a = u & 0x7FFFFFFFu;
+    uint32_t r;
+    if (a > kF32Inf) return kFp8NaN;
+    if (a >= 0x47700000u) {                      // |x| >= 61440 (or Inf)
+        r = (a == kF32Inf) ? 0x7Cu : 0x7Bu;
+    } else if (a < 0x38800000u) {                // |x| < 2^-14
+        r = (uint32_t)__builtin_rintf(__uint_as_float(a) * 65536.0f);
+    } else {
+        uint32_t b = a + 0xFFFFFu + ((a >> 21) & 1u);
+        r = (b >> 21) - (112u << 2);
+    }
+    return r | s;
+}
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).
+struct u32x4 { uint32_t x, y, z, w; };
+
+__device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1) {
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+    const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        uint32_t hi0 = __umulhi(M0, c.x), lo0 = M0 * c.x;
+        uint32_t hi1 = __umulhi(M1, c.z), lo1 = M1 * c.z;
+        u32x4 n;
+        n.x = hi1 ^ c.y ^ k0;
+        n.y = lo1;
+        n.z = hi0 ^ c.w ^ k1;
+        n.w = lo0;
+        c = n;
+        k0 += W0;
+        k1 += W1;
+    }
+    return c;
+}
+
+// Stochastic rounding of a plain float into FP16 (Eq. (1), k' = 23, k = 9):
+// round the magnitude up by one step with probability F / 2^16, where F is
+// the discarded fraction of a step scaled to 16 bits; u16 is uniform on
+// [0, 2^16).  Returns the rounded value as a float and its code.
+struct sr_result { float value; uint16_t code; };
+
+__device__ __forceinline__ sr_result sr16(float x, uint32_t u16) {
+    uint32_t u = __float_as_uint(x);
+    uint32_t s = u & 0x80000000u;
+    uint32_t a = u & 0x7FFFFFFFu;
+    sr_result r;
+    if (a > kF32Inf) { r.value = __uint_as_float(kF32NaN); r.code = kFp16NaN; return r; }
+    if (a >= (97u << 23)) {
+        // normal FP16 range: 14 discarded bits D; F = 4 * D
+        uint32_t up = (u16 < ((a & 0x3FFFu) << 2)) ? 0x4000u : 0u;
+        uint32_t b = (a & 0xFFFFC000u) + up;
+        if (b >= (159u << 23)) {
+            r.value = __uint_as_float(s | kF32Inf);
+            r.code = (uint16_t)((s >> 16) | kFp16Inf);
+        } else {
+            r.value = __uint_as_float(s | b);
+            r.code = (uint16_t)((s >> 16) | ((b >> 14) - (96u << 9)));
+        }
+        return r;
+    }
+    // below 2^-30: fixed step 2^-39
+    float t = __uint_as_float(a) * 0x1p39f;      // exact, < 512
+    float n = __builtin_floorf(t);
+    uint32_t F = (uint32_t)((t - n) * 65536.0f); // exact, floor
+    uint32_t k = (uint32_t)n + ((u16 < F) ? 1u : 0u);
+    r.value = __uint_as_float(s | __float_as_uint((float)k * 0x1p-39f));
+    r.code = (uint16_t)((s >> 16) | k);
+    return r;
+}
+
+}  // namespace fp8t

@@ -1,0 +1,122 @@
+"""The C-ABI library (include/fp8train.h) loads, exports every declared entry
+point, and rejects invalid arguments before touching the GPU.
+
+No compute call is made here: each call below fails validation, which the
+library checks before any HIP call, so these run without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1812_08011_amd as fp8t
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fp8train.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fp8t.LIB_PATH):
+        pytest.skip("libfp8train.so is not built")
+    return fp8t.lib()
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted([
+        "fp8_quantize", "fp16_quantize", "chunk_gemm", "chunk_gemm_workspace_size",
+        "sr_weight_update", "fp8t_status_string"])
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    assert fp8t.status_string(0) == "ok"
+    assert "invalid" in fp8t.status_string(-1)
+    assert "workspace" in fp8t.status_string(-2)
+    assert fp8t.status_string(12345) == "unknown status"
+
+
+FAKE = 0x10000        # never dereferenced: validation fails first
+
+
+def test_fp8_quantize_rejects(lib):
+    assert lib.fp8_quantize(FAKE, 0, 1.0, FAKE, -1, None) == fp8t.EINVAL
+    assert lib.fp8_quantize(FAKE, 7, 1.0, FAKE, 10, None) == fp8t.EINVAL
+    assert lib.fp8_quantize(None, 0, 1.0, FAKE, 10, None) == fp8t.EINVAL
+    assert lib.fp8_quantize(FAKE, 0, 1.0, None, 10, None) == fp8t.EINVAL
+    assert lib.fp8_quantize(None, 0, 1.0, None, 0, None) == fp8t.OK     # empty: no-op
+    assert lib.fp16_quantize(None, FAKE, 5, None) == fp8t.EINVAL
+    assert lib.fp16_quantize(FAKE, FAKE, -5, None) == fp8t.EINVAL
+
+
+def _gemm(lib, **kw):
+    a = dict(ta=0, tb=0, M=4, N=4, K=4, CL=2, A=FAKE, lda=4, B=FAKE, ldb=4, C=FAKE, ldc=4,
+             mode=0, ws=None, wsb=0)
+    a.update(kw)
+    return lib.chunk_gemm(a["ta"], a["tb"], a["M"], a["N"], a["K"], a["CL"], a["A"], a["lda"],
+                          a["B"], a["ldb"], a["C"], a["ldc"], a["mode"], a["ws"], a["wsb"], None)
+
+
+def test_chunk_gemm_rejects(lib):
+    E = fp8t.EINVAL
+    assert _gemm(lib, CL=0) == E
+    assert _gemm(lib, CL=-3) == E
+    assert _gemm(lib, M=-1) == E
+    assert _gemm(lib, K=-1) == E
+    assert _gemm(lib, ta=2) == E
+    assert _gemm(lib, tb=-1) == E
+    assert _gemm(lib, mode=2) == E
+    assert _gemm(lib, lda=3) == E                       # lda < K
+    assert _gemm(lib, ta=1, M=8, lda=4) == E            # lda < M
+    assert _gemm(lib, ldb=3) == E                       # ldb < N
+    assert _gemm(lib, tb=1, K=8, ldb=4, lda=8) == E     # ldb < K
+    assert _gemm(lib, ldc=3) == E
+    assert _gemm(lib, A=None) == E
+    assert _gemm(lib, B=None) == E
+    assert _gemm(lib, C=None) == E
+    assert _gemm(lib, M=2 ** 31) == E                   # beyond 32-bit dimensions
+    assert _gemm(lib, M=0) == fp8t.OK                   # empty output: no-op
+    assert _gemm(lib, N=0, C=None) == fp8t.OK
+
+
+def test_workspace_size_is_zero_for_direct_kernels(lib):
+    assert fp8t.chunk_gemm_workspace_size(0, 0, 128, 128, 1024, 64, 0) == 0
+
+
+def test_sr_weight_update_rejects(lib):
+    E = fp8t.EINVAL
+    f = lib.sr_weight_update
+    assert f(FAKE, FAKE, None, None, 10, 0.1, 0.9, 0.0, 1, 0, None) == E   # momentum, no v
+    assert f(FAKE, FAKE, FAKE, None, -1, 0.1, 0.9, 0.0, 1, 0, None) == E
+    assert f(None, FAKE, None, None, 10, 0.1, 0.0, 0.0, 1, 0, None) == E
+    assert f(FAKE, None, None, None, 10, 0.1, 0.0, 0.0, 1, 0, None) == E
+    assert f(None, None, None, None, 0, 0.1, 0.0, 0.0, 1, 0, None) == fp8t.OK
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(fp8t, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(fp8t, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        fp8t.lib()
+
+
+def test_product_path_does_not_import_the_oracle():
+    pkg = os.path.dirname(fp8t.__file__)
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text, f
+                assert "liboracle" not in text and "oracle.h" not in text, f

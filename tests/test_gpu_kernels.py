@@ -1,0 +1,307 @@
+"""GPU parity: each entry point of libfp8train against the CPU oracle on
+seeded inputs, element by element, at sizes that span several tiles and a
+ragged tail.  Exact-mode GEMMs, quantization and the update must be
+bit-identical; fast-mode GEMMs must lie within the tolerance derived in
+`fast_tolerance` (see below)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1812_08011_amd as fp8t
+from tests.gpu_util import DEV, dev, gemm, host, q8, q16, say
+
+pytestmark = pytest.mark.gpu
+
+U = 2.0 ** -10
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    fp8t.lib()
+    yield
+
+
+def fast_tolerance(absum, K, CL):
+    """Fast mode differs from the fast oracle only in the intra-chunk sums:
+    an FP32 sum of at most CL products (error <= CL * 2^-24 * sum|p|) instead
+    of the exact sum.  Both results are within nch*u*(1+u)^2*sum|p| (+ the FP32
+    term for the GPU) of the exact dot product, u = 2^-10, nch = ceil(K/CL)
+    (recursive summation applied to the chunk roundings and the inter-chunk
+    chain), so they differ by at most twice that."""
+    nch = -(-K // CL) if K else 0
+    cl = min(CL, K) if K else 0
+    return (2 * nch * U * (1 + U) ** 2 + cl * 2.0 ** -24 * (1 + U)) * absum
+
+
+def abs_dot(A_vals, B_vals):
+    """sum_k |a(i,k) b(k,j)| for every output."""
+    return np.abs(A_vals) @ np.abs(B_vals)
+
+
+def check_fast(Cg, Co, absum, K, CL, what):
+    vg, vo = oracle.p16_value(Cg), oracle.p16_value(Co)
+    tol = fast_tolerance(absum, K, CL)
+    both_nan = np.isnan(vg) & np.isnan(vo)
+    same_inf = np.isinf(vg) & (vg == vo)
+    fin = ~(both_nan | same_inf)
+    assert np.all(np.isfinite(vg[fin])), what
+    diff = np.abs(vg[fin] - vo[fin])
+    bad = diff > tol[fin] + 1e-300
+    assert not bad.any(), (what, diff[bad][:5], tol[fin][bad][:5])
+    same = float(np.mean(Cg == Co))
+    say(f"{what}: fast vs fast-oracle bit-identical fraction {same:.4f}")
+    return same
+
+
+# ---- quantization -------------------------------------------------------------
+
+def test_fp8_quantize_f32_bit_patterns():
+    rng = np.random.default_rng(500)
+    bits = rng.integers(0, 2 ** 32, size=2_000_003, dtype=np.uint64).astype(np.uint32)
+    x = np.concatenate([bits.view(np.float32),
+                        rng.standard_normal(1_000_000).astype(np.float32),
+                        (rng.standard_normal(1_000_000) * 1e-5).astype(np.float32)])
+    vals = np.unique(oracle.p8_value(np.arange(0x7C, dtype=np.uint8)))
+    mids = ((vals[1:] + vals[:-1]) / 2).astype(np.float32)
+    x = np.concatenate([x, mids, -mids, np.nextafter(mids, np.float32(np.inf)),
+                        np.nextafter(mids, np.float32(0)),
+                        np.float32([0.0, -0.0, np.inf, -np.inf, np.nan, 61440, 61439.996,
+                                    57344, 1e30, -1e30])])
+    for scale in (1.0, 1000.0, 0.25):
+        say(f"fp8_quantize f32 n={x.size} scale={scale}")
+        got = host(q8(dev(x), scale))
+        ref = oracle.fp8_quantize(x, scale)
+        assert np.array_equal(got, ref), np.flatnonzero(got != ref)[:10]
+
+
+def test_fp8_quantize_all_fp16_codes_and_odd_offsets():
+    codes = np.arange(65536, dtype=np.uint16)
+    for scale in (1.0, 1000.0, 2.0 ** -3):
+        say(f"fp8_quantize fp16 all codes scale={scale}")
+        got = host(q8(dev(codes), scale))
+        assert np.array_equal(got, oracle.fp8_quantize(codes, scale))
+    # misaligned pointers and ragged lengths take the scalar path
+    rng = np.random.default_rng(501)
+    x = rng.standard_normal(10_007).astype(np.float32)
+    xd = dev(x)
+    out = torch.empty(10_007, dtype=torch.uint8, device=DEV)
+    for off in (1, 2, 3):
+        say(f"fp8_quantize misaligned offset {off}")
+        n = x.size - off
+        fp8t.lib().fp8_quantize(xd.data_ptr() + 4 * off, 0, 1.0, out.data_ptr() + off, n,
+                                torch.cuda.current_stream().cuda_stream)
+        got = host(out)[off:off + n]
+        assert np.array_equal(got, oracle.fp8_quantize(x[off:]))
+
+
+def test_fp16_quantize_bit_patterns():
+    rng = np.random.default_rng(502)
+    bits = rng.integers(0, 2 ** 32, size=2_000_001, dtype=np.uint64).astype(np.uint32)
+    vals = oracle.p16_value(np.arange(0x7E00, dtype=np.uint16))
+    mids = ((vals[1:] + vals[:-1]) / 2).astype(np.float32)
+    x = np.concatenate([bits.view(np.float32), mids, -mids,
+                        rng.standard_normal(100_000).astype(np.float32) * np.float32(1e-10),
+                        np.float32([0.0, -0.0, np.inf, -np.inf, np.nan, 4290772992.0,
+                                    4292870144.0, 1e38])])
+    say(f"fp16_quantize n={x.size}")
+    got = host(q16(dev(x)))
+    ref = oracle.fp16_quantize(x)
+    assert np.array_equal(got, ref), np.flatnonzero(got != ref)[:10]
+
+
+# ---- chunk_gemm -----------------------------------------------------------------
+
+SHAPES = [
+    # M, N, K, CL
+    (1, 1, 1, 1),
+    (3, 5, 7, 2),
+    (37, 29, 100, 16),
+    (130, 67, 333, 64),       # ragged in all three dimensions, last chunk 13
+    (64, 128, 256, 64),
+    (257, 131, 129, 1),       # CL = 1: sequential sum
+    (100, 90, 500, 500),      # CL = K: one chunk
+    (45, 61, 300, 1000),      # CL > K
+    (33, 47, 400, 48),        # fast mode: multiple of 16 but not of 64
+    (19, 23, 1030, 256),
+]
+
+
+def _operands(rng, M, N, K, ta, tb, scale=1.0):
+    a = (rng.standard_normal((M, K)) * scale).astype(np.float32)
+    b = rng.standard_normal((K, N)).astype(np.float32)
+    # sprinkle exact zeros, large values and ties
+    a[rng.random(a.shape) < 0.05] = 0.0
+    b[rng.random(b.shape) < 0.02] *= 64.0
+    A = oracle.fp8_quantize(np.ascontiguousarray(a.T if ta else a))
+    B = oracle.fp8_quantize(np.ascontiguousarray(b.T if tb else b))
+    return A, B
+
+
+@pytest.mark.parametrize("tile", ["auto", "1", "2", "4", "8"])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_chunk_gemm_exact_matches_oracle(tile, ta, tb, monkeypatch):
+    if tile != "auto":
+        monkeypatch.setenv("FP8T_VALU_TILE", tile)
+    rng = np.random.default_rng(510 + 2 * ta + tb)
+    for (M, N, K, CL) in SHAPES:
+        A, B = _operands(rng, M, N, K, ta, tb)
+        say(f"chunk_gemm exact tile={tile} ta={ta} tb={tb} M={M} N={N} K={K} CL={CL}")
+        Cg = host(gemm(dev(A), dev(B), M, N, K, CL, ta, tb))
+        Co = oracle.chunk_gemm(A, B, CL, ta, tb)
+        assert np.array_equal(Cg, Co), (M, N, K, CL, np.argwhere(Cg != Co)[:5])
+
+
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_chunk_gemm_fast_within_tolerance(ta, tb):
+    rng = np.random.default_rng(520 + 2 * ta + tb)
+    for (M, N, K, CL) in SHAPES:
+        A, B = _operands(rng, M, N, K, ta, tb)
+        say(f"chunk_gemm fast ta={ta} tb={tb} M={M} N={N} K={K} CL={CL}")
+        Cg = host(gemm(dev(A), dev(B), M, N, K, CL, ta, tb, mode=fp8t.FAST))
+        Co = oracle.chunk_gemm(A, B, CL, ta, tb, mode=oracle.FAST)
+        va = oracle.p8_value(A.T if ta else A)
+        vb = oracle.p8_value(B.T if tb else B)
+        check_fast(Cg, Co, abs_dot(va, vb), K, CL, f"fast {M}x{N}x{K} CL={CL}")
+        if CL == 1:
+            assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, ta, tb))
+
+
+def test_chunk_gemm_padded_leading_dims_and_misaligned_bases():
+    rng = np.random.default_rng(530)
+    M, N, K, CL = 150, 70, 260, 64
+    for ta, tb in ((0, 0), (1, 1), (0, 1), (1, 0)):
+        for off in (0, 1, 3):
+            A, B = _operands(rng, M, N, K, ta, tb)
+            lda, ldb, ldc = A.shape[1] + 5, B.shape[1] + 3, N + 7
+            Ap = np.zeros((A.shape[0], lda + off), np.uint8)
+            Bp = np.zeros((B.shape[0], ldb + off), np.uint8)
+            Ap[:, off:off + A.shape[1]] = A
+            Bp[:, off:off + B.shape[1]] = B
+            Ad, Bd = dev(Ap.ravel()), dev(Bp.ravel())
+            for mode in (fp8t.EXACT, fp8t.FAST):
+                say(f"chunk_gemm padded ta={ta} tb={tb} off={off} mode={mode}")
+                C = dev(np.full((M, ldc), 0xABCD, np.uint16))
+                ldap, ldbp = lda + off, ldb + off
+                fp8t.chunk_gemm(ta, tb, M, N, K, CL, Ad.data_ptr() + off, ldap,
+                                Bd.data_ptr() + off, ldbp, C, ldc, mode)
+                Ch = host(C)
+                assert np.all(Ch[:, N:] == 0xABCD)          # padding untouched
+                Co = oracle.chunk_gemm(A, B, CL, ta, tb, mode=mode)
+                if mode == fp8t.EXACT:
+                    assert np.array_equal(Ch[:, :N], Co)
+                else:
+                    check_fast(Ch[:, :N], Co, abs_dot(oracle.p8_value(A.T if ta else A),
+                                                      oracle.p8_value(B.T if tb else B)),
+                               K, CL, "padded fast")
+
+
+def test_chunk_gemm_degenerate():
+    say("chunk_gemm K=0")
+    C = gemm(dev(np.zeros((5, 1), np.uint8)), dev(np.zeros((1, 7), np.uint8)), 5, 7, 0, 64,
+             lda=1, ldb=7)
+    assert np.all(host(C) == 0)
+    # -0 products give +0; Inf/NaN propagate
+    A = np.array([[0x80, 0x80, 0x80], [0x7C, 0x3C, 0x00], [0x7D, 0x3C, 0x3C],
+                  [0x7B, 0x7B, 0x7B]], np.uint8)
+    B = np.array([[0x3C, 0x3C], [0xFC, 0x3C], [0x3C, 0x7C]], np.uint8)
+    for mode in (fp8t.EXACT, fp8t.FAST):
+        for CL in (1, 2, 16):
+            say(f"chunk_gemm specials mode={mode} CL={CL}")
+            Cg = host(gemm(dev(A), dev(B), 4, 2, 3, CL, mode=mode))
+            assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, mode=mode))
+
+
+def test_chunk_gemm_overflow_to_inf():
+    """Sums beyond the largest FP16 value become Inf and stay Inf."""
+    K = 64 * 40
+    A = np.full((2, K), 0x7B, np.uint8)          # 57344
+    B = np.full((K, 2), 0x7B, np.uint8)
+    B[::2, 1] = 0xFB                              # alternate signs in column 1
+    for mode in (fp8t.EXACT, fp8t.FAST):
+        say(f"chunk_gemm overflow mode={mode}")
+        Cg = host(gemm(dev(A), dev(B), 2, 2, K, 64, mode=mode))
+        Co = oracle.chunk_gemm(A, B, 64, mode=mode)
+        assert np.array_equal(Cg, Co)
+        assert Cg[0, 0] == 0x7E00
+
+
+def test_fig3b_stall_on_gpu():
+    """Sec. 2.3, Fig. 3(b): CL = 1 stalls at exactly 4096, chunking does not."""
+    import workloads
+    x = workloads.accumulation_vector(12000)
+    a = oracle.fp8_quantize(x)[None, :]
+    ones = np.full((12000, 1), 0x3C, np.uint8)
+    for CL in (1, 32, 64, 12000):
+        say(f"fig3b CL={CL}")
+        Cg = host(gemm(dev(a), dev(ones), 1, 1, 12000, CL))
+        assert np.array_equal(Cg, oracle.chunk_gemm(a, ones, CL))
+        if CL in (1, 12000):
+            assert oracle.p16_value(Cg)[0, 0] == 4096.0
+
+
+# ---- sr_weight_update --------------------------------------------------------------
+
+def _update_case(rng, n, with_v=True, with_w8=True, lr=0.1, mu=0.9, wd=1e-4, seed=7, offset=0):
+    w = oracle.fp16_quantize((rng.standard_normal(n) * 0.02).astype(np.float32))
+    g = oracle.fp16_quantize((rng.standard_normal(n) * 1e-4).astype(np.float32))
+    v = oracle.fp16_quantize((rng.standard_normal(n) * 1e-4).astype(np.float32)) if with_v else None
+    wd_, gd = dev(w), dev(g)
+    vd = dev(v) if with_v else None
+    w8d = torch.zeros(n, dtype=torch.uint8, device=DEV) if with_w8 else None
+    say(f"sr_weight_update n={n} v={with_v} w8={with_w8} lr={lr} mu={mu} wd={wd} seed={seed}"
+        f" offset={offset}")
+    fp8t.sr_weight_update(wd_, gd, vd, w8d, n, lr, mu if with_v else 0.0, wd, seed, offset)
+    ow, ov, ow8 = oracle.sr_weight_update(w, g, v, lr=lr, momentum=mu if with_v else 0.0,
+                                          weight_decay=wd, seed=seed, offset=offset,
+                                          want_w8=with_w8)
+    assert np.array_equal(host(wd_), ow)
+    if with_v:
+        assert np.array_equal(host(vd), ov)
+    if with_w8:
+        assert np.array_equal(host(w8d), ow8)
+
+
+def test_sr_update_variants():
+    rng = np.random.default_rng(540)
+    for n in (1, 2, 3, 4097, 100_001):
+        for with_v in (True, False):
+            for with_w8 in (True, False):
+                _update_case(rng, n, with_v, with_w8)
+    _update_case(rng, 50_000, seed=2 ** 63 + 12345, offset=2 ** 40 + 7)
+    _update_case(rng, 50_000, lr=0.0, mu=0.0, wd=0.0)
+
+
+def test_sr_update_misaligned_pointers():
+    rng = np.random.default_rng(541)
+    n = 10_001
+    w = oracle.fp16_quantize((rng.standard_normal(n + 1) * 0.02).astype(np.float32))
+    g = oracle.fp16_quantize((rng.standard_normal(n + 1) * 1e-3).astype(np.float32))
+    wd_, gd = dev(w), dev(g)
+    w8d = torch.zeros(n + 1, dtype=torch.uint8, device=DEV)
+    say("sr_weight_update misaligned")
+    fp8t.lib().sr_weight_update(wd_.data_ptr() + 2, gd.data_ptr() + 2, None,
+                                w8d.data_ptr() + 1, n, 0.1, 0.0, 0.0, 3, 9,
+                                torch.cuda.current_stream().cuda_stream)
+    ow, _, ow8 = oracle.sr_weight_update(w[1:], g[1:], None, lr=0.1, seed=3, offset=9)
+    assert np.array_equal(host(wd_)[1:], ow)
+    assert np.array_equal(host(w8d)[1:], ow8)
+
+
+def test_sr_update_specials():
+    w = np.array([0x7E00, 0xFE00, 0x7F00, 0x0000, 0x8000, 0x0001, 0x7DFF, 0x01FF], np.uint16)
+    g = np.array([0x3C00, 0x3C00, 0x0000, 0x0001, 0x8001, 0x0000, 0xFDFF, 0x0001], np.uint16)
+    v = np.array([0x0000, 0x7E00, 0x0000, 0x0000, 0x0000, 0x0200, 0x0000, 0x0003], np.uint16)
+    wd_, gd, vd = dev(w), dev(g), dev(v)
+    w8d = torch.zeros(8, dtype=torch.uint8, device=DEV)
+    say("sr_weight_update specials")
+    fp8t.sr_weight_update(wd_, gd, vd, w8d, 8, 1.5, 0.9, 1e-4, 1, 2)
+    ow, ov, ow8 = oracle.sr_weight_update(w, g, v, lr=1.5, momentum=0.9, weight_decay=1e-4,
+                                          seed=1, offset=2)
+    assert np.array_equal(host(wd_), ow)
+    assert np.array_equal(host(vd), ov)
+    assert np.array_equal(host(w8d), ow8)

@@ -139,3 +139,23 @@ def test_all_fp8_products_are_exact_in_fp16():
     assert np.array_equal(got[fin], prod[fin])
     assert np.array_equal(np.isnan(got), np.isnan(prod))
     assert np.array_equal(got[np.isinf(prod)], prod[np.isinf(prod)])
+
+
+def test_fp16_quantize_brute_force_nearest():
+    """FP32 -> FP16 round-to-nearest-even, checked by nearest-neighbour search
+    over all FP16 codes, across the subnormal range, ties and overflow."""
+    rng = np.random.default_rng(103)
+    e = rng.uniform(-45.0, 34.0, size=4000)
+    x = (np.sign(rng.standard_normal(e.size)) * np.exp2(e)).astype(np.float32)
+    vals = np.unique(oracle.p16_value(np.arange(0x7E00, dtype=np.uint16)))
+    mids = ((vals[1:] + vals[:-1]) / 2).astype(np.float32)      # exact ties
+    x = np.concatenate([x, rng.choice(mids, 2000), np.float32([0.0, -0.0, np.inf, -np.inf])])
+    got = oracle.fp16_quantize(x)
+    for xi, gi in zip(x.tolist(), got.tolist()):
+        if xi == 0:
+            ref = 0x8000 if np.signbit(xi) else 0
+        elif np.isinf(xi):
+            ref = 0xFE00 if xi < 0 else 0x7E00
+        else:
+            ref = H.brute_rn16(Fraction(xi))
+        assert ref == gi, (xi, hex(gi), hex(ref))
