@@ -1,23 +1,13 @@
 // chunk_gemm: FP8 x FP8 GEMM with chunk-based FP16 accumulation
 // (Sec. 2.3 "Chunk-based Accumulation", dot-product algorithm of Fig. 3(a)).
 //
-// Two kernels:
+// This file holds the C-ABI entry points, the planner that picks a kernel
+// configuration and work decomposition (gemm_plan.h), the fold kernel that
+// finishes tiles whose chunks were shared out, and the matrix-core kernel of
+// the fast mode.  The vector-ALU kernels are in gemm_valu.hip.
 //
-// * chunk_gemm_valu -- the exact mode (and the fast mode for chunk lengths
-//   the matrix cores cannot split).  Every output keeps two registers, the
-//   intra-chunk sum P and the running sum S, in the scaled FP32 domain of
-//   fp8t_device.h.  One multiply-accumulate step is
-//       P = rn16s(fma(a * 2^96, b, P))        (v_fma, v_bfe, v_add3, v_and)
-//   -- the product of two FP8 values is exact in FP32, so the FMA's single
-//   rounding is the rounding of the exact sum -- and at every chunk end
-//       S = rn16s(S + P), P = +0.
-//   This is VALU-bound by construction (gfx950 has no adder for the paper's
-//   FP16), so the kernel is shaped to keep the VALU busy: a TM x TN register
-//   tile per lane, operands staged through LDS already decoded to FP32 (one
-//   decode per element per workgroup tile instead of per use), and a
-//   double-buffered K loop that prefetches the next slab from HBM into
-//   registers while the current slab is consumed.
-//
+// * chunk_gemm_valu (gemm_valu.hip) -- the exact mode, and the fast mode for
+//   chunk lengths the matrix cores cannot split.
 // * chunk_gemm_mfma -- the fast mode for CL a multiple of 16.  FP8 bytes are
 //   the OCP E5M2 ("bf8") encoding (same bias, subnormals and specials), so
 //   the FP8 codes feed v_mfma_f32_32x32x16_bf8_bf8 directly.  Each wave owns a
@@ -26,158 +16,14 @@
 #include "fp8t_device.h"
 #include "fp8train.h"
 #include "fp8t_host.h"
+#include "gemm_plan.h"
+#include "gemm_valu.h"
 
+#include <mutex>
 #include <stdlib.h>
 
 namespace fp8t {
 namespace {
-
-// ---------------------------------------------------------------------------
-// VALU kernel
-// ---------------------------------------------------------------------------
-
-template <int TM, int TN, int LM, int LN, int BK, bool TA, bool TB, bool FAST>
-__global__ __launch_bounds__(LM * LN) void chunk_gemm_valu(
-    int M, int N, int K, int CL, const uint8_t* __restrict__ A, int64_t lda,
-    const uint8_t* __restrict__ B, int64_t ldb, uint16_t* __restrict__ C,
-    int64_t ldc) {
-    constexpr int NT = LM * LN;
-    constexpr int BM = TM * LM;
-    constexpr int BN = TN * LN;
-    constexpr int EA = BM * BK / NT;         // A bytes loaded per thread per slab
-    constexpr int EB = BN * BK / NT;
-    static_assert(EA * NT == BM * BK && EB * NT == BN * BK, "tile/threads mismatch");
-    // pad rows written with a stride across lanes to spread LDS banks
-    constexpr int PA = TA ? 0 : 4;
-    constexpr int PB = TB ? 4 : 0;
-    // A holds a * 2^96 in exact mode (the scaled domain); the fast VALU path
-    // sums plain products in FP32 and scales once per chunk.
-    constexpr int ASHIFT = FAST ? 0 : 96;
-
-    __shared__ float As[2][BK][BM + PA];
-    __shared__ float Bs[2][BK][BN + PB];
-
-    const int tid = threadIdx.x;
-    const int ly = tid / LN, lx = tid % LN;
-    const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-
-    uint32_t ra[EA], rb[EB];
-
-    auto load_slab = [&](int k0) {
-#pragma unroll
-        for (int r = 0; r < EA; ++r) {
-            const int e = tid + NT * r;
-            const int mm = TA ? (e % BM) : (e / BK);
-            const int kk = TA ? (e / BM) : (e % BK);
-            const int m = m0 + mm, k = k0 + kk;
-            uint32_t v = 0;
-            if (m < M && k < K)
-                v = TA ? A[(int64_t)k * lda + m] : A[(int64_t)m * lda + k];
-            ra[r] = v;
-        }
-#pragma unroll
-        for (int r = 0; r < EB; ++r) {
-            const int e = tid + NT * r;
-            const int nn = TB ? (e / BK) : (e % BN);
-            const int kk = TB ? (e % BK) : (e / BN);
-            const int n = n0 + nn, k = k0 + kk;
-            uint32_t v = 0;
-            if (n < N && k < K)
-                v = TB ? B[(int64_t)n * ldb + k] : B[(int64_t)k * ldb + n];
-            rb[r] = v;
-        }
-    };
-    auto store_slab = [&](int buf) {
-#pragma unroll
-        for (int r = 0; r < EA; ++r) {
-            const int e = tid + NT * r;
-            const int mm = TA ? (e % BM) : (e / BK);
-            const int kk = TA ? (e / BM) : (e % BK);
-            As[buf][kk][mm] = fp8_to_f32<ASHIFT>(ra[r]);
-        }
-#pragma unroll
-        for (int r = 0; r < EB; ++r) {
-            const int e = tid + NT * r;
-            const int nn = TB ? (e / BK) : (e % BN);
-            const int kk = TB ? (e % BK) : (e / BN);
-            Bs[buf][kk][nn] = fp8_to_f32<0>(rb[r]);
-        }
-    };
-
-    float P[TM][TN], S[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) { P[i][j] = 0.0f; S[i][j] = 0.0f; }
-
-    auto mac = [&](int buf, int kk) {
-        float a[TM], b[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) a[i] = As[buf][kk][ly * TM + i];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) b[j] = Bs[buf][kk][lx * TN + j];
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                float t = __builtin_fmaf(a[i], b[j], P[i][j]);
-                P[i][j] = FAST ? t : rn16s(t);
-            }
-    };
-    auto flush = [&]() {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                float p = FAST ? rn16s(P[i][j] * 0x1p96f) : P[i][j];
-                S[i][j] = rn16s(S[i][j] + p);
-                P[i][j] = 0.0f;
-            }
-    };
-
-    const int nslabs = (K + BK - 1) / BK;
-    int crem = CL;                  // products left in the current chunk
-    if (nslabs > 0) {
-        load_slab(0);
-        store_slab(0);
-        __syncthreads();
-    }
-    for (int s = 0; s < nslabs; ++s) {
-        const int buf = s & 1;
-        if (s + 1 < nslabs) load_slab((s + 1) * BK);
-        const int kmax = min(BK, K - s * BK);
-        int kk = 0;
-        while (kk < kmax) {
-            const int seg = min(kmax - kk, crem);
-            if (seg == BK) {
-#pragma unroll
-                for (int q = 0; q < BK; ++q) mac(buf, q);
-            } else {
-                for (int q = kk; q < kk + seg; ++q) mac(buf, q);
-            }
-            kk += seg;
-            crem -= seg;
-            if (crem == 0) {
-                flush();
-                crem = CL;
-            }
-        }
-        if (s + 1 < nslabs) store_slab(buf ^ 1);
-        __syncthreads();
-    }
-    if (crem != CL) flush();        // the last, shorter chunk
-
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-        const int m = m0 + ly * TM + i;
-        if (m >= M) continue;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int n = n0 + lx * TN + j;
-            if (n < N) C[(int64_t)m * ldc + n] = f32s_to_fp16(S[i][j]);
-        }
-    }
-}
 
 // ---------------------------------------------------------------------------
 // MFMA kernel (fast mode, CL % 16 == 0)
@@ -372,53 +218,203 @@ __global__ __launch_bounds__(MF_NT) void chunk_gemm_mfma(
 }
 
 // ---------------------------------------------------------------------------
-// host dispatch
+// fold: finish the shared tiles
 // ---------------------------------------------------------------------------
 
-template <int TM, int TN, int LM, int LN, int BK, bool FAST>
-int launch_valu(int ta, int tb, int M, int N, int K, int CL, const uint8_t* A,
-                int64_t lda, const uint8_t* B, int64_t ldb, uint16_t* C, int64_t ldc,
-                hipStream_t stream) {
-    constexpr int BM = TM * LM, BN = TN * LN;
-    dim3 grid((M + BM - 1) / BM, (N + BN - 1) / BN);
-    if (grid.y > 65535u) return FP8T_EINVAL;
-    dim3 block(LM * LN);
-#define FP8T_LAUNCH(TA_, TB_)                                                        \
-    hipLaunchKernelGGL((chunk_gemm_valu<TM, TN, LM, LN, BK, TA_, TB_, FAST>), grid, \
-                       block, 0, stream, M, N, K, CL, A, lda, B, ldb, C, ldc)
-    if (!ta && !tb) FP8T_LAUNCH(false, false);
-    else if (!ta && tb) FP8T_LAUNCH(false, true);
-    else if (ta && !tb) FP8T_LAUNCH(true, false);
-    else FP8T_LAUNCH(true, true);
-#undef FP8T_LAUNCH
-    return launch_status();
+// One thread per output of a shared tile: continue the running sum held in C
+// (the FP16 sum of the tile's first piece) over the chunk sums the other
+// pieces left in the workspace, in ascending chunk order -- the same
+// additions a whole-tile pass makes after its first piece.
+__global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, int BN) {
+    const int64_t per = (int64_t)BM * BN;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t lt = idx / per;
+    if (lt * p.nch >= p.L) return;
+    const int local = (int)(idx - lt * per);
+    const int64_t tile = p.t_whole + lt;
+    const int m = (int)(tile / p.tiles_n) * BM + local / BN;
+    const int n = (int)(tile % p.tiles_n) * BN + local % BN;
+    if (m >= g.M || n >= g.N) return;
+    const int a = first_piece_end(p, lt);
+    if (a >= p.nch) return;
+    uint16_t* cp = g.C + (int64_t)m * g.ldc + n;
+    float S = fp16_to_f32s(*cp);
+    const uint16_t* src = g.ws + lt * p.nch * per + local;
+    int c = a;
+    for (; c + 8 <= p.nch; c += 8) {
+        uint32_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = src[(int64_t)(c + j) * per];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) S = rn16s(S + fp16_to_f32s(v[j]));
+    }
+    for (; c < p.nch; ++c) S = rn16s(S + fp16_to_f32s(src[(int64_t)c * per]));
+    *cp = f32s_to_fp16(S);
 }
 
-template <bool FAST>
-int dispatch_valu(int ta, int tb, int M, int N, int K, int CL, const uint8_t* A,
-                  int64_t lda, const uint8_t* B, int64_t ldb, uint16_t* C, int64_t ldc,
-                  hipStream_t stream) {
-    // FP8T_VALU_TILE = 1, 2, 4 or 8 forces the register tile (for tests and
-    // tuning).  Otherwise: the largest square register tile that still gives
-    // every SIMD (1024 on the chip) at least two waves.
-    const char* force = getenv("FP8T_VALU_TILE");
-    const int t = force ? atoi(force) : 0;
-    if (t == 8)
-        return launch_valu<8, 8, 16, 16, 16, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
-    if (t == 4)
-        return launch_valu<4, 4, 16, 16, 32, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
-    if (t == 2)
-        return launch_valu<2, 2, 16, 16, 32, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
-    if (t == 1)
-        return launch_valu<1, 1, 16, 16, 64, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
-    const int64_t outs = (int64_t)M * N;
-    if (outs / 64 >= 2048 * 64)
-        return launch_valu<8, 8, 16, 16, 16, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
-    if (outs / 16 >= 2048 * 64)
-        return launch_valu<4, 4, 16, 16, 32, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
-    if (outs / 4 >= 2048 * 64)
-        return launch_valu<2, 2, 16, 16, 32, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
-    return launch_valu<1, 1, 16, 16, 64, FAST>(ta, tb, M, N, K, CL, A, lda, B, ldb, C, ldc, stream);
+__global__ void fill_zero_u16(uint16_t* __restrict__ C, int M, int N, int64_t ldc) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t total = (int64_t)M * N;
+    if (i < total) C[(i / N) * ldc + (i % N)] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// planner
+// ---------------------------------------------------------------------------
+
+constexpr double kClockHz = 2.4e9;      // MI355X peak engine clock
+constexpr double kLanesPerCU = 64.0;    // 32-bit VALU lane-ops per clock per CU
+constexpr double kFoldBytesPerS = 4e12; // effective HBM rate of the fold pass
+
+int env_int(const char* name, int dflt) {
+    const char* v = getenv(name);
+    return v ? atoi(v) : dflt;
+}
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static std::mutex mu;
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!cached[dev]) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cached[dev] = n;
+    }
+    return cached[dev];
+}
+
+// Resident workgroups per CU of a kernel (cached per device and kernel).
+int kernel_occupancy(const void* fn, int threads) {
+    static std::mutex mu;
+    struct Ent { int dev; const void* fn; int occ; };
+    static Ent cache[256];
+    static int n = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    std::lock_guard<std::mutex> lk(mu);
+    for (int i = 0; i < n; ++i)
+        if (cache[i].dev == dev && cache[i].fn == fn) return cache[i].occ;
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, threads, 0) != hipSuccess)
+        return 0;
+    if (n < 256) cache[n++] = Ent{dev, fn, occ};
+    return occ;
+}
+
+// VALU lane-ops per multiply-accumulate of each register tile (4 for the
+// rounded FMA, plus LDS reads and loop overhead that grow as tiles shrink).
+double valu_ops_per_mac(const ValuShape& s) {
+    const int t = s.TM * s.TN;
+    if (t >= 64) return 4.1;
+    if (t >= 32) return 4.15;
+    if (t >= 16) return 4.3;
+    if (t >= 4) return 5.5;
+    return 9.0;
+}
+
+struct Choice {
+    int cfg = -1;
+    ValuShape shape{};
+    Plan plan{};
+    size_t ws_bytes = 0;
+    double est_s = 0.0;
+};
+
+constexpr size_t kWsAlign = 256;
+
+// The best configuration for these sizes; with allow_ws false only plans
+// that need no workspace are considered.
+Choice plan_valu(int ta, int tb, int fast, int64_t M, int64_t N, int64_t K, int64_t CL,
+                 bool allow_ws) {
+    Choice best;
+    const int cus = device_cus();
+    if (cus <= 0) return best;
+    // Overrides for tests and tuning: the register tile, a cap on the
+    // workgroups, and 1 / 0 to require / forbid shared tiles.
+    int force_cfg = env_int("FP8T_VALU_TILE", -1);
+    if (force_cfg >= 0 && (force_cfg >= kValuConfigs || !valu_kernel(force_cfg, ta, tb, fast)))
+        force_cfg = -1;                      // not built for this mode: plan freely
+    const int force_g = env_int("FP8T_GEMM_WGS", 0);
+    const int force_split = env_int("FP8T_GEMM_SPLIT", -1);
+    const int64_t nch = (K + CL - 1) / CL;
+    for (int cfg = 0; cfg < kValuConfigs; ++cfg) {
+        if (force_cfg >= 0 && cfg != force_cfg) continue;
+        if (force_cfg < 0 && cfg == 0) continue;      // cfg 0 is kept for comparison only
+        const ValuShape sh = valu_shape(cfg);
+        const void* fn = valu_kernel(cfg, ta, tb, fast);
+        if (!fn) continue;
+        int occ = kernel_occupancy(fn, sh.NT);
+        if (occ <= 0) continue;
+        if (occ > 8) occ = 8;
+        const int64_t tiles_m = (M + sh.BM - 1) / sh.BM;
+        const int64_t tiles_n = (N + sh.BN - 1) / sh.BN;
+        const int64_t T = tiles_m * tiles_n;
+        int64_t gmax = (int64_t)cus * occ;
+        if (force_g > 0 && force_g < gmax) gmax = force_g;
+        // Rate of one CU on this tile, derated when few waves share a SIMD.
+        const double eff = occ >= 3 ? 1.0 : (occ == 2 ? 0.9 : 0.6);
+        const double t_chunk = (double)sh.BM * sh.BN * (double)CL * valu_ops_per_mac(sh) /
+                               (kLanesPerCU * kClockHz * eff);     // one tile-chunk on a CU
+        for (int split = 0; split < 2; ++split) {
+            if (split && !allow_ws) continue;
+            if (force_split == 0 && split) continue;
+            Plan p{};
+            p.tiles_n = tiles_n;
+            p.nch = (int)nch;
+            double est;
+            size_t ws = 0;
+            if (!split) {
+                const int64_t G = T < gmax ? T : gmax;
+                p.G = (int)G;
+                p.t_whole = T;
+                p.L = 0;
+                // tile-chunks on the busiest CU
+                const int64_t per_cu = (T + cus - 1) / cus;
+                est = (double)per_cu * nch * t_chunk;
+            } else {
+                int64_t G = gmax;
+                if (G > T * nch) G = T * nch;
+                const int64_t q = T / G;
+                p.G = (int)G;
+                p.t_whole = q * G;
+                p.L = (T - p.t_whole) * nch;
+                if (p.L == 0) continue;                    // same as the plain plan
+                const int64_t wg_per_cu = (G + cus - 1) / cus;
+                const int64_t per_wg = q * nch + (p.L + G - 1) / G;
+                ws = (size_t)(T - p.t_whole) * nch * sh.BM * sh.BN * sizeof(uint16_t) + kWsAlign;
+                est = (double)wg_per_cu * per_wg * t_chunk + 2.0 * (double)ws / kFoldBytesPerS +
+                      4e-6;
+            }
+            if (force_split == 1 && !split && allow_ws) est *= 1e6;   // any shared plan wins
+            if (best.cfg < 0 || est < best.est_s) {
+                best.cfg = cfg;
+                best.shape = sh;
+                best.plan = p;
+                best.ws_bytes = ws;
+                best.est_s = est;
+            }
+        }
+    }
+    return best;
+}
+
+int launch_valu_plan(const Choice& ch, int ta, int tb, int fast, GemmArgs g,
+                     hipStream_t stream) {
+    void* args[] = {&g, const_cast<Plan*>(&ch.plan)};
+    if (hipLaunchKernel(valu_kernel(ch.cfg, ta, tb, fast), dim3(ch.plan.G),
+                        dim3(ch.shape.NT), args, 0, stream) != hipSuccess)
+        return FP8T_EHIP;
+    if (ch.plan.L > 0) {
+        const int64_t shared = ch.plan.L / ch.plan.nch;
+        const int64_t threads = shared * ch.shape.BM * ch.shape.BN;
+        hipLaunchKernelGGL(chunk_fold, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                           stream, g, ch.plan, ch.shape.BM, ch.shape.BN);
+    }
+    return launch_status();
 }
 
 int dispatch_mfma(int ta, int tb, int M, int N, int K, int CL, const uint8_t* A,
@@ -445,11 +441,6 @@ int dispatch_mfma(int ta, int tb, int M, int N, int K, int CL, const uint8_t* A,
     return launch_status();
 }
 
-__global__ void fill_zero_u16(uint16_t* __restrict__ C, int M, int N, int64_t ldc) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const int64_t total = (int64_t)M * N;
-    if (i < total) C[(i / N) * ldc + (i % N)] = 0;
-}
 
 }  // namespace
 }  // namespace fp8t
@@ -465,19 +456,26 @@ bool gemm_args_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, i
     if (M > INT32_MAX || N > INT32_MAX || K > INT32_MAX) return false;
     return true;
 }
+
+bool uses_mfma(int mode, int64_t K, int64_t CL) {
+    const int64_t cl = CL > K ? K : CL;
+    return mode == FP8T_FAST && cl % 16 == 0;
+}
 }  // namespace
 
 extern "C" size_t chunk_gemm_workspace_size(int trans_a, int trans_b, int64_t M,
                                             int64_t N, int64_t K, int64_t CL, int mode) {
-    (void)trans_a; (void)trans_b; (void)M; (void)N; (void)K; (void)CL; (void)mode;
-    return 0;
+    if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, mode)) return 0;
+    if (M == 0 || N == 0 || K == 0 || uses_mfma(mode, K, CL)) return 0;
+    const int64_t cl = CL > K ? K : CL;
+    const Choice ch = plan_valu(trans_a, trans_b, mode == FP8T_FAST, M, N, K, cl, true);
+    return ch.cfg < 0 ? 0 : ch.ws_bytes;
 }
 
 extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                           int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
                           int64_t ldb, uint16_t* C, int64_t ldc, int mode,
                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    (void)workspace;
     if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, mode)) return FP8T_EINVAL;
     if (M == 0 || N == 0) return FP8T_OK;
     if (!C || ldc < N) return FP8T_EINVAL;
@@ -485,8 +483,7 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
         if (!A || !B) return FP8T_EINVAL;
         if (lda < (trans_a ? M : K) || ldb < (trans_b ? K : N)) return FP8T_EINVAL;
     }
-    if (workspace_bytes < chunk_gemm_workspace_size(trans_a, trans_b, M, N, K, CL, mode))
-        return FP8T_EWORKSPACE;
+    if (workspace_bytes > 0 && !workspace) return FP8T_EINVAL;
     if (CL > K && K > 0) CL = K;           // one chunk
     const int m = (int)M, n = (int)N, k = (int)K, cl = (int)(K > 0 ? CL : 1);
     if (K == 0) {
@@ -495,9 +492,33 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
                            0, stream, C, m, n, ldc);
         return launch_status();
     }
-    if (mode == FP8T_FAST && cl % 16 == 0)
+    if (uses_mfma(mode, K, cl))
         return dispatch_mfma(trans_a, trans_b, m, n, k, cl, A, lda, B, ldb, C, ldc, stream);
-    if (mode == FP8T_FAST)
-        return dispatch_valu<true>(trans_a, trans_b, m, n, k, cl, A, lda, B, ldb, C, ldc, stream);
-    return dispatch_valu<false>(trans_a, trans_b, m, n, k, cl, A, lda, B, ldb, C, ldc, stream);
+
+    const int fast = mode == FP8T_FAST;
+    // With no workspace, the best plan that needs none; with one, the best
+    // plan overall, which must then fit.
+    Choice ch = plan_valu(trans_a, trans_b, fast, M, N, K, cl, workspace_bytes > 0);
+    if (ch.cfg < 0) return FP8T_EHIP;
+    if (ch.ws_bytes > workspace_bytes) return FP8T_EWORKSPACE;
+    GemmArgs g{};
+    g.A = A;
+    g.B = B;
+    g.C = C;
+    g.ws = nullptr;
+    if (ch.plan.L > 0) {
+        const uintptr_t base = ((uintptr_t)workspace + kWsAlign - 1) & ~(uintptr_t)(kWsAlign - 1);
+        g.ws = reinterpret_cast<uint16_t*>(base);
+    }
+    g.lda = lda;
+    g.ldb = ldb;
+    g.ldc = ldc;
+    g.M = m;
+    g.N = n;
+    g.K = k;
+    g.CL = cl;
+    g.a_vec = aligned(A, 4) && lda % 4 == 0;
+    g.b_vec = aligned(B, 4) && ldb % 4 == 0;
+    g.c_vec = aligned(C, 4) && ldc % 2 == 0;
+    return launch_valu_plan(ch, trans_a, trans_b, fast, g, stream);
 }

@@ -67,6 +67,20 @@ __device__ __forceinline__ float fp16_to_f32(uint32_t c) {
     return __uint_as_float(bits | ((c & 0x8000u) << 16));
 }
 
+// FP16 code -> scaled-domain float (value * 2^96, exact).
+__device__ __forceinline__ float fp16_to_f32s(uint32_t c) {
+    uint32_t e = (c >> 9) & 63u, m = c & 511u;
+    uint32_t bits;
+    if (e == 63u) {
+        bits = m ? kF32NaN : kF32Inf;
+    } else if (e == 0u) {
+        bits = __float_as_uint((float)m * 0x1p57f);
+    } else {
+        bits = ((c & 0x7FFFu) << 14) + (192u << 23);
+    }
+    return __uint_as_float(bits | ((c & 0x8000u) << 16));
+}
+
 // Scaled-domain float already on the FP16 grid (low 14 bits zero) -> code.
 __device__ __forceinline__ uint16_t f32s_to_fp16(float x) {
     uint32_t u = __float_as_uint(x);

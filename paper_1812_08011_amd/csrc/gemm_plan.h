@@ -1,0 +1,57 @@
+// Work decomposition shared by the chunk_gemm kernels.
+//
+// The output is cut into BM x BN tiles numbered row-major (t = tm * tiles_n +
+// tn).  A tile's K range is cut into nch chunks of CL products starting at
+// k = 0 (Sec. 2.3: chunks are independent until their sums are added, in
+// order, into the running sum).  A launch has G workgroups:
+//
+//   * tiles [0, t_whole) are processed whole, workgroup w taking tiles
+//     w, w + G, w + 2G, ...: the chunk sums go straight into the running sum
+//     and the FP16 result into C;
+//   * the remaining T - t_whole tiles, laid end to end as L = (T - t_whole) *
+//     nch tile-chunks, are shared out as contiguous ranges
+//     [w * L / G, (w + 1) * L / G), so every workgroup ends with the same
+//     number of chunks.  A range piece that starts at chunk 0 of its tile
+//     writes the running sum of its chunks to C; a piece that starts later
+//     writes each chunk's FP16 sum to the workspace, and chunk_fold then
+//     continues the running sum from C over those chunk sums in ascending
+//     order.  The additions are the same ones, in the same order, as when a
+//     tile is processed whole, so the result does not depend on the plan.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fp8t {
+
+struct GemmArgs {
+    const uint8_t* A;
+    const uint8_t* B;
+    uint16_t* C;
+    uint16_t* ws;       // chunk sums of the shared tiles (null when L == 0)
+    int64_t lda, ldb, ldc;
+    int M, N, K, CL;
+    int a_vec;          // A, lda allow 4-byte loads
+    int b_vec;          // B, ldb allow 4-byte loads
+    int c_vec;          // C, ldc allow stores of a lane's whole row of codes
+};
+
+struct Plan {
+    int64_t tiles_n;
+    int64_t t_whole;
+    int64_t L;          // tile-chunks shared out
+    int nch;            // chunks per tile
+    int G;              // workgroups
+};
+
+// First chunk of shared tile lt that the workspace holds: the end of the
+// piece that starts at the tile's chunk 0 (nch if the tile is not split).
+__host__ __device__ inline int first_piece_end(const Plan& p, int64_t lt) {
+    const int64_t x = lt * p.nch;                       // tile start
+    const int64_t w0 = ((x + 1) * p.G - 1) / p.L;       // range holding x
+    const int64_t e = (w0 + 1) * p.L / p.G;             // its end
+    const int64_t a = e - x;
+    return a < p.nch ? (int)a : p.nch;
+}
+
+}  // namespace fp8t

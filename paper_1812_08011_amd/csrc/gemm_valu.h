@@ -1,0 +1,26 @@
+// Vector-ALU chunk_gemm kernels (gemm_valu.hip): register-tile shapes and
+// kernel entry addresses, for the host-side planner in chunk_gemm.hip.
+#pragma once
+
+#include "gemm_plan.h"
+
+namespace fp8t {
+
+struct ValuShape {
+    int TM, TN;     // outputs per lane
+    int BM, BN;     // outputs per workgroup
+    int NT;         // threads per workgroup
+};
+
+constexpr int kValuConfigs = 7;
+
+ValuShape valu_shape(int cfg);
+
+// __global__ function of register-tile configuration cfg (0 .. kValuConfigs-1)
+// for the given operand layouts and mode (fast: sum a chunk in FP32 and round
+// once), taking (GemmArgs, Plan); null where that variant is not built (the
+// fast variants exist for the small tiles only: the fast mode runs here only
+// for chunk lengths the matrix cores cannot split).
+const void* valu_kernel(int cfg, int ta, int tb, int fast);
+
+}  // namespace fp8t

@@ -1,0 +1,31 @@
+// Dispatch tables of the vector-ALU chunk_gemm kernels (gemm_valu_impl.h).
+#include "gemm_valu_impl.h"
+
+namespace fp8t {
+
+const void* valu_kernel_nn(int cfg, int fast);
+const void* valu_kernel_nt(int cfg, int fast);
+const void* valu_kernel_tn(int cfg, int fast);
+const void* valu_kernel_tt(int cfg, int fast);
+
+ValuShape valu_shape(int cfg) {
+    switch (cfg) {
+        case 0: return valu_impl::shape_of<0>();
+        case 1: return valu_impl::shape_of<1>();
+        case 2: return valu_impl::shape_of<2>();
+        case 3: return valu_impl::shape_of<3>();
+        case 4: return valu_impl::shape_of<4>();
+        case 5: return valu_impl::shape_of<5>();
+        default: return valu_impl::shape_of<6>();
+    }
+}
+
+const void* valu_kernel(int cfg, int ta, int tb, int fast) {
+    if (cfg < 0 || cfg >= kValuConfigs) return nullptr;
+    if (!ta && !tb) return valu_kernel_nn(cfg, fast);
+    if (!ta && tb) return valu_kernel_nt(cfg, fast);
+    if (ta && !tb) return valu_kernel_tn(cfg, fast);
+    return valu_kernel_tt(cfg, fast);
+}
+
+}  // namespace fp8t

@@ -1,0 +1,368 @@
+// chunk_gemm on the vector ALUs: the exact mode, and the fast mode for chunk
+// lengths that are not a multiple of the matrix-core K step.
+//
+// Every output keeps two registers, the intra-chunk sum P and the running sum
+// S, in the scaled FP32 domain of fp8t_device.h.  One multiply-accumulate of
+// the dot product of Sec. 2.3 / Fig. 3(a) is
+//     P = rn16s(fma(a * 2^96, b, P))        (v_fmac, v_bfe, v_add3, v_and)
+// -- an FP8 x FP8 product is exact in FP32, so the FMA's one rounding is the
+// rounding of the exact sum -- and at every chunk end
+//     S = rn16s(S + P), P = +0.
+// gfx950 has no adder for the paper's FP16, so this is bound by the VALU
+// issue rate: 4 instructions per multiply-accumulate.  The kernel is shaped
+// to issue little else:
+//   * a TM x TN register tile per lane; operands are staged through LDS
+//     already decoded to FP32 (one decode per element per workgroup tile);
+//   * K slabs of BK are double-buffered in LDS, the next slab is fetched from
+//     HBM (4-byte loads where alignment allows) while the current one is
+//     consumed, and with PF the LDS reads of step k+1 are issued before the
+//     arithmetic of step k so their latency is hidden;
+//   * a persistent grid of exactly as many workgroups as fit on the chip,
+//     sharing out tiles and chunks evenly (gemm_plan.h), so no CU idles in a
+//     last partial wave of workgroups.
+#pragma once
+
+#include <type_traits>
+
+#include "fp8t_device.h"
+#include "gemm_valu.h"
+
+namespace fp8t {
+namespace valu_impl {
+
+// One operand slab of a workgroup: rows [r0, r0 + R) of the operand's row
+// index (m for A, n for B) by k in [k0, k0 + BK), clipped to `rows` and
+// `kend`.  KC: k is the contiguous index in memory (element (r, k) at
+// p[r * ld + k]); otherwise the row index is (element at p[k * ld + r]).  Each
+// of the NT threads holds W words of 4 consecutive bytes between the HBM load
+// and the LDS store; `vec` allows 4-byte loads (aligned base and ld).
+template <bool KC, int R, int BK, int NT, int W>
+__device__ __forceinline__ void slab_load(const uint8_t* __restrict__ ptr, int64_t ld,
+                                          int vec, int r0, int rows, int k0, int kend,
+                                          int tid, uint32_t (&reg)[W]) {
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int d = tid + NT * w;
+        int r, k;
+        if (KC) { r = d / (BK / 4); k = (d % (BK / 4)) * 4; }
+        else    { k = d / (R / 4);  r = (d % (R / 4)) * 4; }
+        const int gr = r0 + r, gk = k0 + k;
+        uint32_t v = 0;
+        if (KC) {
+            if (gr < rows && gk < kend) {
+                const uint8_t* q = ptr + (int64_t)gr * ld + gk;
+                if (vec && gk + 3 < kend) {
+                    v = *reinterpret_cast<const uint32_t*>(q);
+                } else {
+                    for (int b = 0; b < 4; ++b)
+                        if (gk + b < kend) v |= (uint32_t)q[b] << (8 * b);
+                }
+            }
+        } else {
+            if (gk < kend && gr < rows) {
+                const uint8_t* q = ptr + (int64_t)gk * ld + gr;
+                if (vec && gr + 3 < rows) {
+                    v = *reinterpret_cast<const uint32_t*>(q);
+                } else {
+                    for (int b = 0; b < 4; ++b)
+                        if (gr + b < rows) v |= (uint32_t)q[b] << (8 * b);
+                }
+            }
+        }
+        reg[w] = v;
+    }
+}
+
+// Decode a thread's words into the LDS slab, laid out [k][row] with `pitch`
+// floats per k; SH = 96 writes the scaled domain.
+template <bool KC, int R, int BK, int NT, int W, int SH>
+__device__ __forceinline__ void slab_store(float* lds, int pitch, int tid,
+                                           const uint32_t (&reg)[W]) {
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int d = tid + NT * w;
+        const uint32_t v = reg[w];
+        if (KC) {
+            const int r = d / (BK / 4), k = (d % (BK / 4)) * 4;
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+                lds[(k + b) * pitch + r] = fp8_to_f32<SH>((v >> (8 * b)) & 0xFFu);
+        } else {
+            const int k = d / (R / 4), r = (d % (R / 4)) * 4;
+            float4 f;
+            f.x = fp8_to_f32<SH>(v & 0xFFu);
+            f.y = fp8_to_f32<SH>((v >> 8) & 0xFFu);
+            f.z = fp8_to_f32<SH>((v >> 16) & 0xFFu);
+            f.w = fp8_to_f32<SH>(v >> 24);
+            *reinterpret_cast<float4*>(&lds[k * pitch + r]) = f;
+        }
+    }
+}
+
+template <int TM, int TN, int LM, int LN, int BK, bool PF, int WPE, bool TA, bool TB, bool FAST>
+__global__ __launch_bounds__(LM * LN) __attribute__((amdgpu_waves_per_eu(WPE)))
+void chunk_gemm_valu(GemmArgs g, Plan p) {
+    constexpr int NT = LM * LN;
+    constexpr int BM = TM * LM;
+    constexpr int BN = TN * LN;
+    // 4-byte words per thread per slab
+    constexpr int WA = BM * BK / 4 / NT;
+    constexpr int WB = BN * BK / 4 / NT;
+    static_assert(WA * NT * 4 == BM * BK && WB * NT * 4 == BN * BK, "tile/threads mismatch");
+    static_assert(BK % 4 == 0 && BM % 4 == 0 && BN % 4 == 0, "tile must hold whole words");
+    static_assert(TN == 1 || TN % 2 == 0, "codes are stored in pairs");
+    // padding of rows written with a stride across lanes (spreads LDS banks)
+    constexpr int PA = TA ? 0 : 4;
+    constexpr int PB = TB ? 4 : 0;
+    // A holds a * 2^96 in exact mode (the scaled domain); the fast VALU path
+    // sums plain products in FP32 and scales once per chunk.
+    constexpr int ASHIFT = FAST ? 0 : 96;
+    constexpr bool KCA = !TA;      // A is k-contiguous unless transposed
+    constexpr bool KCB = TB;       // B is k-contiguous only when transposed
+
+    __shared__ __attribute__((aligned(16))) float As[2][BK][BM + PA];
+    __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + PB];
+
+    const int tid = threadIdx.x;
+    const int ly = tid / LN, lx = tid % LN;
+
+    uint32_t ra[WA], rb[WB];
+    float P[TM][TN], S[TM][TN];
+
+    auto fma_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                float t = __builtin_fmaf(a[i], b[j], P[i][j]);
+                P[i][j] = FAST ? t : rn16s(t);
+            }
+    };
+    auto lds_read = [&](float (&a)[TM], float (&b)[TN], int buf, int kk) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) a[i] = As[buf][kk][ly * TM + i];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) b[j] = Bs[buf][kk][lx * TN + j];
+    };
+
+    // One piece: chunks [c0, c1) of tile `tile`.  lt >= 0 marks a shared tile
+    // (its index among the shared tiles), whose chunk sums go to the workspace
+    // when the piece does not start at chunk 0.
+    auto piece = [&](int64_t tile, int c0, int c1, int64_t lt) __attribute__((always_inline)) {
+        const int m0 = (int)(tile / p.tiles_n) * BM;
+        const int n0 = (int)(tile % p.tiles_n) * BN;
+        const int kbeg = (int)((int64_t)c0 * g.CL);
+        const int64_t kend64 = (int64_t)c1 * g.CL;
+        const int kend = kend64 < g.K ? (int)kend64 : g.K;
+        const bool to_ws = c0 > 0;
+        int chunk = c0;
+
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) { P[i][j] = 0.0f; S[i][j] = 0.0f; }
+
+        auto flush = [&]() __attribute__((always_inline)) {
+            if (to_ws) {
+                uint16_t* dst = g.ws + ((lt * p.nch + chunk) * BM + ly * TM) * BN + lx * TN;
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    uint32_t w[(TN + 1) / 2];
+#pragma unroll
+                    for (int j = 0; j < TN; j += 2) {
+                        float p0 = FAST ? rn16s(P[i][j] * 0x1p96f) : P[i][j];
+                        uint32_t c = f32s_to_fp16(p0);
+                        if (j + 1 < TN) {
+                            float p1 = FAST ? rn16s(P[i][j + 1] * 0x1p96f) : P[i][j + 1];
+                            c |= (uint32_t)f32s_to_fp16(p1) << 16;
+                        }
+                        w[j / 2] = c;
+                    }
+                    if (TN == 1) {
+                        dst[i * BN] = (uint16_t)w[0];
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < TN / 2; ++j)
+                            reinterpret_cast<uint32_t*>(dst + i * BN)[j] = w[j];
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) {
+                        float pv = FAST ? rn16s(P[i][j] * 0x1p96f) : P[i][j];
+                        S[i][j] = rn16s(S[i][j] + pv);
+                    }
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) P[i][j] = 0.0f;
+            ++chunk;
+        };
+
+        const int nk = kend - kbeg;
+        const int nslabs = (nk + BK - 1) / BK;
+        int crem = g.CL;                 // products left in the current chunk
+        slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, kbeg, kend, tid, ra);
+        slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, kbeg, kend, tid, rb);
+        slab_store<KCA, BM, BK, NT, WA, ASHIFT>(&As[0][0][0], BM + PA, tid, ra);
+        slab_store<KCB, BN, BK, NT, WB, 0>(&Bs[0][0][0], BN + PB, tid, rb);
+        __syncthreads();
+        for (int s = 0; s < nslabs; ++s) {
+            const int buf = s & 1;
+            const int ks = kbeg + s * BK;
+            if (s + 1 < nslabs) {
+                slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, ks + BK, kend, tid, ra);
+                slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, ks + BK, kend, tid, rb);
+            }
+            const int kmax = min(BK, kend - ks);
+            int kk = 0;
+            while (kk < kmax) {
+                const int seg = min(kmax - kk, crem);
+                if (seg == BK) {
+                    if (PF) {
+                        float a0[TM], b0[TN], a1[TM], b1[TN];
+                        lds_read(a0, b0, buf, 0);
+#pragma unroll
+                        for (int q = 0; q < BK; q += 2) {
+                            lds_read(a1, b1, buf, q + 1);
+                            fma_step(a0, b0);
+                            if (q + 2 < BK) lds_read(a0, b0, buf, q + 2);
+                            fma_step(a1, b1);
+                        }
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < BK; ++q) {
+                            float a[TM], b[TN];
+                            lds_read(a, b, buf, q);
+                            fma_step(a, b);
+                        }
+                    }
+                } else {
+                    for (int q = kk; q < kk + seg; ++q) {
+                        float a[TM], b[TN];
+                        lds_read(a, b, buf, q);
+                        fma_step(a, b);
+                    }
+                }
+                kk += seg;
+                crem -= seg;
+                if (crem == 0) {
+                    flush();
+                    crem = g.CL;
+                }
+            }
+            if (s + 1 < nslabs) {
+                slab_store<KCA, BM, BK, NT, WA, ASHIFT>(&As[buf ^ 1][0][0], BM + PA, tid, ra);
+                slab_store<KCB, BN, BK, NT, WB, 0>(&Bs[buf ^ 1][0][0], BN + PB, tid, rb);
+            }
+            __syncthreads();
+        }
+        if (crem != g.CL) flush();       // the last, shorter chunk
+
+        if (to_ws) return;
+        // The running sum: a lane's TN consecutive codes of a row are one
+        // vector store when the whole row lies inside C and is aligned.
+        const int nl = n0 + lx * TN;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int m = m0 + ly * TM + i;
+            if (m >= g.M) continue;
+            uint16_t* crow = g.C + (int64_t)m * g.ldc + nl;
+            if (TN > 1 && g.c_vec && nl + TN <= g.N) {
+#pragma unroll
+                for (int j = 0; j < TN; j += 2) {
+                    uint32_t c = (uint32_t)f32s_to_fp16(S[i][j]) |
+                                 ((uint32_t)f32s_to_fp16(S[i][j + 1]) << 16);
+                    reinterpret_cast<uint32_t*>(crow)[j / 2] = c;
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    if (nl + j < g.N) crow[j] = f32s_to_fp16(S[i][j]);
+            }
+        }
+    };
+
+    // Work items of this workgroup: whole tiles, then its range of the
+    // shared tile-chunks (gemm_plan.h).  One call site keeps one copy of the
+    // piece code.
+    const int w = blockIdx.x;
+    int64_t t = w;
+    int64_t s = p.L > 0 ? (int64_t)w * p.L / p.G : 0;
+    const int64_t e = p.L > 0 ? (int64_t)(w + 1) * p.L / p.G : 0;
+    for (;;) {
+        int64_t tile, lt;
+        int c0, c1;
+        if (t < p.t_whole) {
+            tile = t;
+            lt = -1;
+            c0 = 0;
+            c1 = p.nch;
+            t += p.G;
+        } else if (s < e) {
+            lt = s / p.nch;
+            c0 = (int)(s - lt * p.nch);
+            const int64_t c1l = e - lt * p.nch;
+            c1 = c1l < p.nch ? (int)c1l : p.nch;
+            tile = p.t_whole + lt;
+            s = lt * p.nch + c1;
+        } else {
+            break;
+        }
+        piece(tile, c0, c1, lt);
+    }
+}
+
+// Register tiles: TM x TN outputs per lane, lane grid LM x LN, K slab BK,
+// LDS prefetch PF, and the waves per SIMD the register budget must allow.
+template <int C> struct ValuCfg;
+template <> struct ValuCfg<0> { static constexpr int TM = 8, TN = 8, LM = 16, LN = 16, BK = 16, WPE = 2; static constexpr bool PF = false; };
+template <> struct ValuCfg<1> { static constexpr int TM = 8, TN = 8, LM = 16, LN = 16, BK = 16, WPE = 2; static constexpr bool PF = true; };
+template <> struct ValuCfg<2> { static constexpr int TM = 8, TN = 4, LM = 16, LN = 16, BK = 16, WPE = 3; static constexpr bool PF = true; };
+template <> struct ValuCfg<3> { static constexpr int TM = 4, TN = 8, LM = 16, LN = 16, BK = 16, WPE = 3; static constexpr bool PF = true; };
+template <> struct ValuCfg<4> { static constexpr int TM = 4, TN = 4, LM = 16, LN = 16, BK = 32, WPE = 4; static constexpr bool PF = true; };
+template <> struct ValuCfg<5> { static constexpr int TM = 2, TN = 2, LM = 16, LN = 16, BK = 32, WPE = 8; static constexpr bool PF = false; };
+template <> struct ValuCfg<6> { static constexpr int TM = 1, TN = 1, LM = 16, LN = 16, BK = 64, WPE = 8; static constexpr bool PF = false; };
+
+template <int C, bool TA, bool TB, bool FAST>
+const void* kernel_of() {
+    using Q = ValuCfg<C>;
+    return reinterpret_cast<const void*>(
+        &chunk_gemm_valu<Q::TM, Q::TN, Q::LM, Q::LN, Q::BK, Q::PF, Q::WPE, TA, TB, FAST>);
+}
+
+// Entry addresses of every configuration for one operand layout; the fast
+// variants exist for the configurations from kValuFastFirst on.
+template <bool TA, bool TB>
+const void* kernel_table(int cfg, int fast) {
+    if (fast) {
+        switch (cfg) {
+            case 4: return kernel_of<4, TA, TB, true>();
+            case 5: return kernel_of<5, TA, TB, true>();
+            case 6: return kernel_of<6, TA, TB, true>();
+            default: return nullptr;
+        }
+    }
+    switch (cfg) {
+        case 0: return kernel_of<0, TA, TB, false>();
+        case 1: return kernel_of<1, TA, TB, false>();
+        case 2: return kernel_of<2, TA, TB, false>();
+        case 3: return kernel_of<3, TA, TB, false>();
+        case 4: return kernel_of<4, TA, TB, false>();
+        case 5: return kernel_of<5, TA, TB, false>();
+        case 6: return kernel_of<6, TA, TB, false>();
+        default: return nullptr;
+    }
+}
+
+template <int C>
+ValuShape shape_of() {
+    using Q = ValuCfg<C>;
+    return ValuShape{Q::TM, Q::TN, Q::TM * Q::LM, Q::TN * Q::LN, Q::LM * Q::LN};
+}
+
+}  // namespace valu_impl
+}  // namespace fp8t

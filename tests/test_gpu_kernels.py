@@ -142,7 +142,10 @@ def _operands(rng, M, N, K, ta, tb, scale=1.0):
     return A, B
 
 
-@pytest.mark.parametrize("tile", ["auto", "1", "2", "4", "8"])
+VALU_TILES = ["auto", "0", "1", "2", "3", "4", "5", "6"]
+
+
+@pytest.mark.parametrize("tile", VALU_TILES)
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_chunk_gemm_exact_matches_oracle(tile, ta, tb, monkeypatch):
     if tile != "auto":
@@ -154,6 +157,63 @@ def test_chunk_gemm_exact_matches_oracle(tile, ta, tb, monkeypatch):
         Cg = host(gemm(dev(A), dev(B), M, N, K, CL, ta, tb))
         Co = oracle.chunk_gemm(A, B, CL, ta, tb)
         assert np.array_equal(Cg, Co), (M, N, K, CL, np.argwhere(Cg != Co)[:5])
+
+
+# Shapes whose tiles get shared out over few workgroups: tiles split at chunk
+# boundaries, pieces of one chunk, ragged last chunks, shared and whole tiles
+# in one launch.
+SPLIT_SHAPES = [
+    # M, N, K, CL
+    (130, 67, 333, 64),
+    (200, 150, 1000, 16),
+    (64, 64, 4096, 64),
+    (33, 47, 700, 48),
+    (17, 300, 64, 8),
+]
+
+
+@pytest.mark.parametrize("tile", ["1", "2", "4", "5", "6"])
+@pytest.mark.parametrize("wgs", ["1", "3", "7", "50"])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (1, 0), (0, 1)])
+def test_chunk_gemm_exact_shared_tiles(tile, wgs, ta, tb, monkeypatch):
+    """Every plan (whole tiles, shared tiles continued by the fold pass) gives
+    the oracle's bits: the chunk sums and their order do not depend on it."""
+    monkeypatch.setenv("FP8T_VALU_TILE", tile)
+    monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
+    monkeypatch.setenv("FP8T_GEMM_SPLIT", "1")
+    rng = np.random.default_rng(550 + 2 * ta + tb)
+    for (M, N, K, CL) in SPLIT_SHAPES:
+        A, B = _operands(rng, M, N, K, ta, tb)
+        ws = fp8t.chunk_gemm_workspace_size(ta, tb, M, N, K, CL, fp8t.EXACT)
+        say(f"chunk_gemm exact shared tile={tile} wgs={wgs} ta={ta} tb={tb} M={M} N={N} "
+            f"K={K} CL={CL} ws={ws}")
+        Cg = host(gemm(dev(A), dev(B), M, N, K, CL, ta, tb))
+        Co = oracle.chunk_gemm(A, B, CL, ta, tb)
+        assert np.array_equal(Cg, Co), (M, N, K, CL, np.argwhere(Cg != Co)[:5])
+
+
+def test_chunk_gemm_workspace_contract():
+    """No workspace: a plan that needs none, same bits.  Too small a
+    workspace is rejected before anything is enqueued."""
+    rng = np.random.default_rng(560)
+    M, N, K, CL = 96, 200, 2048, 64
+    A, B = _operands(rng, M, N, K, 0, 0)
+    Ad, Bd = dev(A), dev(B)
+    Co = oracle.chunk_gemm(A, B, CL)
+    ws = fp8t.chunk_gemm_workspace_size(0, 0, M, N, K, CL, fp8t.EXACT)
+    say(f"workspace contract ws={ws}")
+    C = torch.empty((M, N), dtype=torch.uint16, device=DEV)
+    fp8t.chunk_gemm(0, 0, M, N, K, CL, Ad, K, Bd, N, C, N, fp8t.EXACT)
+    assert np.array_equal(host(C), Co)
+    if ws > 0:
+        small = torch.empty(ws - 1, dtype=torch.uint8, device=DEV)
+        with pytest.raises(fp8t.Fp8tError) as e:
+            fp8t.chunk_gemm(0, 0, M, N, K, CL, Ad, K, Bd, N, C, N, fp8t.EXACT, small, ws - 1)
+        assert e.value.status == fp8t.EWORKSPACE
+        big = torch.full((ws,), 0xA5, dtype=torch.uint8, device=DEV)
+        C.fill_(0)
+        fp8t.chunk_gemm(0, 0, M, N, K, CL, Ad, K, Bd, N, C, N, fp8t.EXACT, big, ws)
+        assert np.array_equal(host(C), Co)
 
 
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
