@@ -520,5 +520,7 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
     g.a_vec = aligned(A, 4) && lda % 4 == 0;
     g.b_vec = aligned(B, 4) && ldb % 4 == 0;
     g.c_vec = aligned(C, 4) && ldc % 2 == 0;
+    // FP8T_GEMM_GUARD=0 runs every piece on the safe path (tests, tuning).
+    g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
     return launch_valu_plan(ch, trans_a, trans_b, fast, g, stream);
 }

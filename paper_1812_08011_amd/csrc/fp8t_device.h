@@ -93,6 +93,35 @@ __device__ __forceinline__ uint16_t f32s_to_fp16(float x) {
     return (uint16_t)(s | k);
 }
 
+// Float in the domain scaled by 2^S, already on the FP16 grid -> code
+// (S = 96: the scaled domain above; S = 64: the guarded domain of the exact
+// GEMM's fast path).  An FP16 value 2^(e-31) (1 + m/512) has FP32 exponent
+// field e + S + 96 there.
+template <int S>
+__device__ __forceinline__ uint16_t f32d_to_fp16(float x) {
+    uint32_t u = __float_as_uint(x);
+    uint32_t s = (u >> 16) & 0x8000u;
+    uint32_t a = u & 0x7FFFFFFFu;
+    if (a > kF32Inf) return kFp16NaN;
+    if (a >= (uint32_t)(S + 159) << 23) return (uint16_t)(s | kFp16Inf);   // >= 2^(32+S)
+    if (a >= (uint32_t)(S + 97) << 23)                                      // >= 2^(S-30)
+        return (uint16_t)(s | ((a >> 14) - ((uint32_t)(S + 96) << 9)));
+    uint32_t k = (uint32_t)(__uint_as_float(a) * __builtin_ldexpf(1.0f, 39 - S));
+    return (uint16_t)(s | k);
+}
+
+// Round to a 10-bit significand, ties to even, by Veltkamp splitting
+// (c = x (2^14 + 1), hi = c - (c - x)): three full-rate VALU operations.
+// Valid when x (2^14 + 1) neither overflows nor leaves the normal range --
+// for the GEMM's guarded domain (|x| in [2^25, 2^96) or 0) it always holds.
+// Equality with integer round-to-nearest-even is checked exhaustively over
+// whole binades of both signs in the tests.
+__device__ __forceinline__ float rn16v(float x) {
+    const float c = x * 16385.0f;
+    const float d = c - x;
+    return c - d;
+}
+
 // Plain float -> nearest FP16 code, ties to even; overflow -> Inf.
 __device__ __forceinline__ uint16_t f32_to_fp16_rn(float x) {
     uint32_t u = __float_as_uint(x);

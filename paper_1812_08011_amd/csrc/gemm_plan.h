@@ -34,6 +34,7 @@ struct GemmArgs {
     int a_vec;          // A, lda allow 4-byte loads
     int b_vec;          // B, ldb allow 4-byte loads
     int c_vec;          // C, ldc allow stores of a lane's whole row of codes
+    int guarded;        // exact mode: try the guarded path first
 };
 
 struct Plan {

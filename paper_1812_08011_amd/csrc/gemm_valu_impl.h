@@ -2,15 +2,27 @@
 // lengths that are not a multiple of the matrix-core K step.
 //
 // Every output keeps two registers, the intra-chunk sum P and the running sum
-// S, in the scaled FP32 domain of fp8t_device.h.  One multiply-accumulate of
-// the dot product of Sec. 2.3 / Fig. 3(a) is
-//     P = rn16s(fma(a * 2^96, b, P))        (v_fmac, v_bfe, v_add3, v_and)
-// -- an FP8 x FP8 product is exact in FP32, so the FMA's one rounding is the
-// rounding of the exact sum -- and at every chunk end
-//     S = rn16s(S + P), P = +0.
+// S, as FP32 values on the FP16 grid.  One multiply-accumulate of the dot
+// product of Sec. 2.3 / Fig. 3(a) is one FMA -- an FP8 x FP8 product is exact
+// in FP32, so its one rounding is the rounding of the exact sum -- followed
+// by rounding to the 10-bit FP16 significand; at every chunk end
+//     S = round(S + P), P = +0.
+// The double rounding 24 -> 10 bits is innocuous since 24 >= 2*10 + 2.
 // gfx950 has no adder for the paper's FP16, so this is bound by the VALU
-// issue rate: 4 instructions per multiply-accumulate.  The kernel is shaped
-// to issue little else:
+// issue rate.  Two paths compute the same bits:
+//   * guarded (default): values scaled by 2^64, rounding by Veltkamp
+//     splitting (rn16v: v_mul, v_sub, v_sub) -- 4 full-rate instructions per
+//     multiply-accumulate.  It holds when no operand is Inf/NaN and no
+//     partial sum can reach the FP16 overflow threshold: every partial sum of
+//     the two-level chain is at most 9 sum_k |a_k b_k| (an RN step adds at
+//     most 3x its non-negative addend, over two levels), so
+//     9 K max|a| max|b| < 2^31 suffices.  Each workgroup tracks the largest
+//     operand code while decoding and checks this at the end of a piece;
+//   * safe: values scaled by 2^96, which maps FP16 overflow onto FP32
+//     overflow, rounding on the raw bits (rn16s: v_bfe, v_add3, v_and).  A
+//     piece that fails the check is recomputed this way (chunk sums in the
+//     workspace are simply rewritten; C is written only after the check).
+// The kernel is shaped to issue little else:
 //   * a TM x TN register tile per lane; operands are staged through LDS
 //     already decoded to FP32 (one decode per element per workgroup tile);
 //   * K slabs of BK are double-buffered in LDS, the next slab is fetched from
@@ -74,14 +86,19 @@ __device__ __forceinline__ void slab_load(const uint8_t* __restrict__ ptr, int64
 }
 
 // Decode a thread's words into the LDS slab, laid out [k][row] with `pitch`
-// floats per k; SH = 96 writes the scaled domain.
-template <bool KC, int R, int BK, int NT, int W, int SH>
+// floats per k, each value times 2^SH; TRACK keeps the largest magnitude code
+// seen in mcode.
+template <bool KC, int R, int BK, int NT, int W, int SH, bool TRACK>
 __device__ __forceinline__ void slab_store(float* lds, int pitch, int tid,
-                                           const uint32_t (&reg)[W]) {
+                                           const uint32_t (&reg)[W], uint32_t& mcode) {
 #pragma unroll
     for (int w = 0; w < W; ++w) {
         const int d = tid + NT * w;
         const uint32_t v = reg[w];
+        if (TRACK) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) mcode = max(mcode, (v >> (8 * b)) & 0x7Fu);
+        }
         if (KC) {
             const int r = d / (BK / 4), k = (d % (BK / 4)) * 4;
 #pragma unroll
@@ -114,14 +131,15 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
     // padding of rows written with a stride across lanes (spreads LDS banks)
     constexpr int PA = TA ? 0 : 4;
     constexpr int PB = TB ? 4 : 0;
-    // A holds a * 2^96 in exact mode (the scaled domain); the fast VALU path
-    // sums plain products in FP32 and scales once per chunk.
-    constexpr int ASHIFT = FAST ? 0 : 96;
     constexpr bool KCA = !TA;      // A is k-contiguous unless transposed
     constexpr bool KCB = TB;       // B is k-contiguous only when transposed
+    // The guarded path exists for the exact mode; the fast mode's VALU
+    // variant (chunks summed in plain FP32, rounded once) always runs safe.
+    constexpr bool HAS_GUARDED = !FAST;
 
     __shared__ __attribute__((aligned(16))) float As[2][BK][BM + PA];
     __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + PB];
+    __shared__ uint32_t s_mcode[2];
 
     const int tid = threadIdx.x;
     const int ly = tid / LN, lx = tid % LN;
@@ -129,15 +147,6 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
     uint32_t ra[WA], rb[WB];
     float P[TM][TN], S[TM][TN];
 
-    auto fma_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                float t = __builtin_fmaf(a[i], b[j], P[i][j]);
-                P[i][j] = FAST ? t : rn16s(t);
-            }
-    };
     auto lds_read = [&](float (&a)[TM], float (&b)[TN], int buf, int kk) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < TM; ++i) a[i] = As[buf][kk][ly * TM + i];
@@ -147,8 +156,18 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 
     // One piece: chunks [c0, c1) of tile `tile`.  lt >= 0 marks a shared tile
     // (its index among the shared tiles), whose chunk sums go to the workspace
-    // when the piece does not start at chunk 0.
-    auto piece = [&](int64_t tile, int c0, int c1, int64_t lt) __attribute__((always_inline)) {
+    // when the piece does not start at chunk 0.  SAFE selects the path (see
+    // the top of this file); the guarded path returns false, having written
+    // nothing to C, when its check fails.
+    auto piece = [&](auto safe_tag, int64_t tile, int c0, int c1, int64_t lt)
+                     __attribute__((always_inline)) -> bool {
+        constexpr bool SAFE = decltype(safe_tag)::value;
+        // value scale of the path: 2^96 (safe, exact), 2^64 (guarded); the
+        // fast mode's VALU variant sums plain products and scales per chunk
+        constexpr int DOM = SAFE ? 96 : 64;
+        constexpr int ASHIFT = FAST ? 0 : DOM;
+        constexpr bool TRACK = !SAFE;
+
         const int m0 = (int)(tile / p.tiles_n) * BM;
         const int n0 = (int)(tile % p.tiles_n) * BN;
         const int kbeg = (int)((int64_t)c0 * g.CL);
@@ -156,6 +175,23 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         const int kend = kend64 < g.K ? (int)kend64 : g.K;
         const bool to_ws = c0 > 0;
         int chunk = c0;
+        uint32_t mca = 0, mcb = 0;           // largest magnitude codes seen
+
+        auto rnd = [&](float x) __attribute__((always_inline)) -> float {
+            return SAFE ? rn16s(x) : rn16v(x);
+        };
+        auto chunk_value = [&](float x) __attribute__((always_inline)) -> float {
+            return FAST ? rn16s(x * 0x1p96f) : x;
+        };
+        auto fma_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    float t = __builtin_fmaf(a[i], b[j], P[i][j]);
+                    P[i][j] = FAST ? t : rnd(t);
+                }
+        };
 
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -170,12 +206,9 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                     uint32_t w[(TN + 1) / 2];
 #pragma unroll
                     for (int j = 0; j < TN; j += 2) {
-                        float p0 = FAST ? rn16s(P[i][j] * 0x1p96f) : P[i][j];
-                        uint32_t c = f32s_to_fp16(p0);
-                        if (j + 1 < TN) {
-                            float p1 = FAST ? rn16s(P[i][j + 1] * 0x1p96f) : P[i][j + 1];
-                            c |= (uint32_t)f32s_to_fp16(p1) << 16;
-                        }
+                        uint32_t c = f32d_to_fp16<DOM>(chunk_value(P[i][j]));
+                        if (j + 1 < TN)
+                            c |= (uint32_t)f32d_to_fp16<DOM>(chunk_value(P[i][j + 1])) << 16;
                         w[j / 2] = c;
                     }
                     if (TN == 1) {
@@ -190,10 +223,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
-                    for (int j = 0; j < TN; ++j) {
-                        float pv = FAST ? rn16s(P[i][j] * 0x1p96f) : P[i][j];
-                        S[i][j] = rn16s(S[i][j] + pv);
-                    }
+                    for (int j = 0; j < TN; ++j) S[i][j] = rnd(S[i][j] + chunk_value(P[i][j]));
             }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
@@ -207,8 +237,8 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         int crem = g.CL;                 // products left in the current chunk
         slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, kbeg, kend, tid, ra);
         slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, kbeg, kend, tid, rb);
-        slab_store<KCA, BM, BK, NT, WA, ASHIFT>(&As[0][0][0], BM + PA, tid, ra);
-        slab_store<KCB, BN, BK, NT, WB, 0>(&Bs[0][0][0], BN + PB, tid, rb);
+        slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[0][0][0], BM + PA, tid, ra, mca);
+        slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[0][0][0], BN + PB, tid, rb, mcb);
         __syncthreads();
         for (int s = 0; s < nslabs; ++s) {
             const int buf = s & 1;
@@ -255,16 +285,32 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                 }
             }
             if (s + 1 < nslabs) {
-                slab_store<KCA, BM, BK, NT, WA, ASHIFT>(&As[buf ^ 1][0][0], BM + PA, tid, ra);
-                slab_store<KCB, BN, BK, NT, WB, 0>(&Bs[buf ^ 1][0][0], BN + PB, tid, rb);
+                slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[buf ^ 1][0][0], BM + PA, tid, ra, mca);
+                slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[buf ^ 1][0][0], BN + PB, tid, rb, mcb);
             }
             __syncthreads();
         }
         if (crem != g.CL) flush();       // the last, shorter chunk
 
-        if (to_ws) return;
-        // The running sum: a lane's TN consecutive codes of a row are one
-        // vector store when the whole row lies inside C and is aligned.
+        if (!SAFE) {
+            // Largest codes over the workgroup's operands of this piece.  The
+            // bound uses the full K, so that pieces of one tile that each pass
+            // bound the whole chain together.
+            if (tid == 0) { s_mcode[0] = 0; s_mcode[1] = 0; }
+            __syncthreads();
+            atomicMax(&s_mcode[0], mca);
+            atomicMax(&s_mcode[1], mcb);
+            __syncthreads();
+            const uint32_t ca = s_mcode[0], cb = s_mcode[1];
+            __syncthreads();                 // s_mcode is reused by the next piece
+            if (ca >= 0x7Cu || cb >= 0x7Cu) return false;       // Inf or NaN operand
+            const double bound = 9.0 * (double)g.K * (double)fp8_to_f32<0>(ca) *
+                                 (double)fp8_to_f32<0>(cb);
+            if (!(bound < 2147483648.0)) return false;         // 2^31
+        }
+        if (to_ws) return true;
+        // The running sum: a lane's TN consecutive codes of a row are stored
+        // in pairs when the whole row lies inside C and is aligned.
         const int nl = n0 + lx * TN;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
@@ -274,21 +320,22 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             if (TN > 1 && g.c_vec && nl + TN <= g.N) {
 #pragma unroll
                 for (int j = 0; j < TN; j += 2) {
-                    uint32_t c = (uint32_t)f32s_to_fp16(S[i][j]) |
-                                 ((uint32_t)f32s_to_fp16(S[i][j + 1]) << 16);
+                    uint32_t c = (uint32_t)f32d_to_fp16<DOM>(S[i][j]) |
+                                 ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 1]) << 16);
                     reinterpret_cast<uint32_t*>(crow)[j / 2] = c;
                 }
             } else {
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    if (nl + j < g.N) crow[j] = f32s_to_fp16(S[i][j]);
+                    if (nl + j < g.N) crow[j] = f32d_to_fp16<DOM>(S[i][j]);
             }
         }
+        return true;
     };
 
     // Work items of this workgroup: whole tiles, then its range of the
-    // shared tile-chunks (gemm_plan.h).  One call site keeps one copy of the
-    // piece code.
+    // shared tile-chunks (gemm_plan.h).  One call site per path keeps one
+    // copy of each path's code.
     const int w = blockIdx.x;
     int64_t t = w;
     int64_t s = p.L > 0 ? (int64_t)w * p.L / p.G : 0;
@@ -312,7 +359,10 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         } else {
             break;
         }
-        piece(tile, c0, c1, lt);
+        bool done = false;
+        if (HAS_GUARDED && g.guarded)
+            done = piece(std::integral_constant<bool, false>{}, tile, c0, c1, lt);
+        if (!done) piece(std::integral_constant<bool, true>{}, tile, c0, c1, lt);
     }
 }
 

@@ -145,15 +145,20 @@ def _operands(rng, M, N, K, ta, tb, scale=1.0):
 VALU_TILES = ["auto", "0", "1", "2", "3", "4", "5", "6"]
 
 
+@pytest.mark.parametrize("guard", ["1", "0"])
 @pytest.mark.parametrize("tile", VALU_TILES)
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
-def test_chunk_gemm_exact_matches_oracle(tile, ta, tb, monkeypatch):
+def test_chunk_gemm_exact_matches_oracle(tile, ta, tb, guard, monkeypatch):
+    """Both paths of the exact kernel (guarded: scaled by 2^64 with Veltkamp
+    rounding; safe: scaled by 2^96 with integer rounding) on every tile."""
     if tile != "auto":
         monkeypatch.setenv("FP8T_VALU_TILE", tile)
+    monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
     rng = np.random.default_rng(510 + 2 * ta + tb)
     for (M, N, K, CL) in SHAPES:
         A, B = _operands(rng, M, N, K, ta, tb)
-        say(f"chunk_gemm exact tile={tile} ta={ta} tb={tb} M={M} N={N} K={K} CL={CL}")
+        say(f"chunk_gemm exact tile={tile} guard={guard} ta={ta} tb={tb} M={M} N={N} K={K} "
+            f"CL={CL}")
         Cg = host(gemm(dev(A), dev(B), M, N, K, CL, ta, tb))
         Co = oracle.chunk_gemm(A, B, CL, ta, tb)
         assert np.array_equal(Cg, Co), (M, N, K, CL, np.argwhere(Cg != Co)[:5])
@@ -274,6 +279,26 @@ def test_chunk_gemm_degenerate():
             say(f"chunk_gemm specials mode={mode} CL={CL}")
             Cg = host(gemm(dev(A), dev(B), 4, 2, 3, CL, mode=mode))
             assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, mode=mode))
+
+
+def test_chunk_gemm_guard_falls_back_per_piece(monkeypatch):
+    """Tiles whose operands could overflow (or hold Inf/NaN) fail the guarded
+    path's check and are recomputed on the safe path, in the same launch as
+    tiles that pass; shared tiles mix both paths across their pieces."""
+    rng = np.random.default_rng(570)
+    M, N, K, CL = 300, 140, 1536, 64
+    A, B = _operands(rng, M, N, K, 0, 0)
+    A[5, :] = 0x7B                      # 57344: 9 K max|a| max|b| far above 2^31
+    A[200, 700] = 0xFC                  # -Inf
+    B[:, 3] = np.where(rng.random(K) < 0.5, 0x7A, 0xFA)   # +-49152
+    Co = oracle.chunk_gemm(A, B, CL)
+    for split in ("0", "1"):
+        for wgs in ("0", "7"):
+            monkeypatch.setenv("FP8T_GEMM_SPLIT", split)
+            monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
+            say(f"guard fallback split={split} wgs={wgs}")
+            Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
+            assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
 
 
 def test_chunk_gemm_overflow_to_inf():
