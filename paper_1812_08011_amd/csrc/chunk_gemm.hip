@@ -20,6 +20,7 @@
 #include "gemm_valu.h"
 
 #include <mutex>
+#include <stdio.h>
 #include <stdlib.h>
 
 namespace fp8t {
@@ -263,7 +264,7 @@ __global__ void fill_zero_u16(uint16_t* __restrict__ C, int M, int N, int64_t ld
 // ---------------------------------------------------------------------------
 
 constexpr double kClockHz = 2.4e9;      // MI355X peak engine clock
-constexpr double kLanesPerCU = 64.0;    // 32-bit VALU lane-ops per clock per CU
+constexpr double kLanesPerCU = 128.0;   // 32-bit VALU lane-ops per clock per CU
 constexpr double kFoldBytesPerS = 4e12; // effective HBM rate of the fold pass
 
 int env_int(const char* name, int dflt) {
@@ -305,15 +306,20 @@ int kernel_occupancy(const void* fn, int threads) {
     return occ;
 }
 
-// VALU lane-ops per multiply-accumulate of each register tile (4 for the
-// rounded FMA, plus LDS reads and loop overhead that grow as tiles shrink).
-double valu_ops_per_mac(const ValuShape& s) {
-    const int t = s.TM * s.TN;
-    if (t >= 64) return 4.1;
-    if (t >= 32) return 4.15;
-    if (t >= 16) return 4.3;
-    if (t >= 4) return 5.5;
-    return 9.0;
+// Relative cost per multiply-accumulate of each register tile on a fully
+// loaded CU, in VALU instructions (4 for the rounded FMA of the guarded path,
+// plus operand decode, LDS reads, loop overhead and lost occupancy; measured
+// on the conv-stage GEMMs for the large tiles).
+double valu_ops_per_mac(int cfg) {
+    switch (cfg) {
+        case 4: return 4.6;     // 4 x 4, 4 waves per SIMD
+        case 3: return 4.85;    // 4 x 8
+        case 2: return 4.9;     // 8 x 4
+        case 1: return 5.1;     // 8 x 8, 2 waves per SIMD
+        case 0: return 5.2;
+        case 5: return 6.5;     // 2 x 2
+        default: return 10.0;   // 1 x 1
+    }
 }
 
 struct Choice {
@@ -355,10 +361,9 @@ Choice plan_valu(int ta, int tb, int fast, int64_t M, int64_t N, int64_t K, int6
         const int64_t T = tiles_m * tiles_n;
         int64_t gmax = (int64_t)cus * occ;
         if (force_g > 0 && force_g < gmax) gmax = force_g;
-        // Rate of one CU on this tile, derated when few waves share a SIMD.
-        const double eff = occ >= 3 ? 1.0 : (occ == 2 ? 0.9 : 0.6);
-        const double t_chunk = (double)sh.BM * sh.BN * (double)CL * valu_ops_per_mac(sh) /
-                               (kLanesPerCU * kClockHz * eff);     // one tile-chunk on a CU
+        // time of one tile-chunk on a CU
+        const double t_chunk = (double)sh.BM * sh.BN * (double)CL * valu_ops_per_mac(cfg) /
+                               (kLanesPerCU * kClockHz);
         for (int split = 0; split < 2; ++split) {
             if (split && !allow_ws) continue;
             if (force_split == 0 && split) continue;
@@ -390,6 +395,10 @@ Choice plan_valu(int ta, int tb, int fast, int64_t M, int64_t N, int64_t K, int6
                       4e-6;
             }
             if (force_split == 1 && !split && allow_ws) est *= 1e6;   // any shared plan wins
+            if (env_int("FP8T_GEMM_VERBOSE", 0))
+                fprintf(stderr, "[fp8t plan] cfg %d occ %d split %d G %d T %lld t_whole %lld L %lld "
+                        "ws %zu est %.1f us\n", cfg, occ, split, p.G, (long long)T,
+                        (long long)p.t_whole, (long long)p.L, ws, est * 1e6);
             if (best.cfg < 0 || est < best.est_s) {
                 best.cfg = cfg;
                 best.shape = sh;

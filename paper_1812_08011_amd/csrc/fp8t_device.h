@@ -94,8 +94,7 @@ __device__ __forceinline__ uint16_t f32s_to_fp16(float x) {
 }
 
 // Float in the domain scaled by 2^S, already on the FP16 grid -> code
-// (S = 96: the scaled domain above; S = 64: the guarded domain of the exact
-// GEMM's fast path).  An FP16 value 2^(e-31) (1 + m/512) has FP32 exponent
+// (S = 96: the scaled domain above; S = 0: plain values).  An FP16 value 2^(e-31) (1 + m/512) has FP32 exponent
 // field e + S + 96 there.
 template <int S>
 __device__ __forceinline__ uint16_t f32d_to_fp16(float x) {
@@ -113,7 +112,7 @@ __device__ __forceinline__ uint16_t f32d_to_fp16(float x) {
 // Round to a 10-bit significand, ties to even, by Veltkamp splitting
 // (c = x (2^14 + 1), hi = c - (c - x)): three full-rate VALU operations.
 // Valid when x (2^14 + 1) neither overflows nor leaves the normal range --
-// for the GEMM's guarded domain (|x| in [2^25, 2^96) or 0) it always holds.
+// for the GEMM's guarded path (|x| in [2^-39, 2^31] or 0) it always holds.
 // Equality with integer round-to-nearest-even is checked exhaustively over
 // whole binades of both signs in the tests.
 __device__ __forceinline__ float rn16v(float x) {

@@ -10,14 +10,16 @@
 // The double rounding 24 -> 10 bits is innocuous since 24 >= 2*10 + 2.
 // gfx950 has no adder for the paper's FP16, so this is bound by the VALU
 // issue rate.  Two paths compute the same bits:
-//   * guarded (default): values scaled by 2^64, rounding by Veltkamp
-//     splitting (rn16v: v_mul, v_sub, v_sub) -- 4 full-rate instructions per
-//     multiply-accumulate.  It holds when no operand is Inf/NaN and no
+//   * guarded (default): plain values, rounding by Veltkamp splitting
+//     (rn16v: v_mul, v_sub, v_sub) -- 4 full-rate instructions per
+//     multiply-accumulate (FP16 subnormals are FP32-normal, so no scaling is
+//     needed when nothing can overflow).  It holds when no operand is Inf/NaN and no
 //     partial sum can reach the FP16 overflow threshold: every partial sum of
 //     the two-level chain is at most 9 sum_k |a_k b_k| (an RN step adds at
 //     most 3x its non-negative addend, over two levels), so
 //     9 K max|a| max|b| < 2^31 suffices.  Each workgroup tracks the largest
-//     operand code while decoding and checks this at the end of a piece;
+//     operand magnitude and any Inf/NaN code while decoding, and checks this
+//     at the end of a piece;
 //   * safe: values scaled by 2^96, which maps FP16 overflow onto FP32
 //     overflow, rounding on the raw bits (rn16s: v_bfe, v_add3, v_and).  A
 //     piece that fails the check is recomputed this way (chunk sums in the
@@ -86,32 +88,41 @@ __device__ __forceinline__ void slab_load(const uint8_t* __restrict__ ptr, int64
 }
 
 // Decode a thread's words into the LDS slab, laid out [k][row] with `pitch`
-// floats per k, each value times 2^SH; TRACK keeps the largest magnitude code
-// seen in mcode.
+// floats per k, each value times 2^SH.  The FP8 codes are the OCP E5M2
+// ("bf8") encoding (bias 15, gradual underflow, exponent 31 for Inf/NaN), so
+// the hardware conversion decodes two of them per instruction, exactly.
+// TRACK keeps the largest magnitude decoded (amax) and flags any Inf/NaN
+// code (special: nonzero iff some byte has an all-ones exponent field).
 template <bool KC, int R, int BK, int NT, int W, int SH, bool TRACK>
 __device__ __forceinline__ void slab_store(float* lds, int pitch, int tid,
-                                           const uint32_t (&reg)[W], uint32_t& mcode) {
+                                           const uint32_t (&reg)[W], float& amax,
+                                           uint32_t& special) {
+    typedef float v2f __attribute__((ext_vector_type(2)));
 #pragma unroll
     for (int w = 0; w < W; ++w) {
         const int d = tid + NT * w;
         const uint32_t v = reg[w];
+        const v2f lo = __builtin_amdgcn_cvt_pk_f32_bf8((int)v, false);
+        const v2f hi = __builtin_amdgcn_cvt_pk_f32_bf8((int)v, true);
+        float f[4] = {lo.x, lo.y, hi.x, hi.y};
         if (TRACK) {
+            // exponent field 0x7C in a byte: adding 0x04 sets its top bit,
+            // and no smaller field carries into the next byte
+            special |= ((v & 0x7C7C7C7Cu) + 0x04040404u) & 0x80808080u;
 #pragma unroll
-            for (int b = 0; b < 4; ++b) mcode = max(mcode, (v >> (8 * b)) & 0x7Fu);
+            for (int b = 0; b < 4; ++b) amax = fmaxf(amax, fabsf(f[b]));
+        }
+        if (SH != 0) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) f[b] *= __builtin_ldexpf(1.0f, SH);   // exact
         }
         if (KC) {
             const int r = d / (BK / 4), k = (d % (BK / 4)) * 4;
 #pragma unroll
-            for (int b = 0; b < 4; ++b)
-                lds[(k + b) * pitch + r] = fp8_to_f32<SH>((v >> (8 * b)) & 0xFFu);
+            for (int b = 0; b < 4; ++b) lds[(k + b) * pitch + r] = f[b];
         } else {
             const int k = d / (R / 4), r = (d % (R / 4)) * 4;
-            float4 f;
-            f.x = fp8_to_f32<SH>(v & 0xFFu);
-            f.y = fp8_to_f32<SH>((v >> 8) & 0xFFu);
-            f.z = fp8_to_f32<SH>((v >> 16) & 0xFFu);
-            f.w = fp8_to_f32<SH>(v >> 24);
-            *reinterpret_cast<float4*>(&lds[k * pitch + r]) = f;
+            *reinterpret_cast<float4*>(&lds[k * pitch + r]) = make_float4(f[0], f[1], f[2], f[3]);
         }
     }
 }
@@ -139,7 +150,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 
     __shared__ __attribute__((aligned(16))) float As[2][BK][BM + PA];
     __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + PB];
-    __shared__ uint32_t s_mcode[2];
+    __shared__ uint32_t s_track[3];     // |a| max bits, |b| max bits, specials
 
     const int tid = threadIdx.x;
     const int ly = tid / LN, lx = tid % LN;
@@ -162,9 +173,9 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
     auto piece = [&](auto safe_tag, int64_t tile, int c0, int c1, int64_t lt)
                      __attribute__((always_inline)) -> bool {
         constexpr bool SAFE = decltype(safe_tag)::value;
-        // value scale of the path: 2^96 (safe, exact), 2^64 (guarded); the
+        // value scale of the path: 2^96 (safe, exact), 1 (guarded); the
         // fast mode's VALU variant sums plain products and scales per chunk
-        constexpr int DOM = SAFE ? 96 : 64;
+        constexpr int DOM = SAFE ? 96 : 0;
         constexpr int ASHIFT = FAST ? 0 : DOM;
         constexpr bool TRACK = !SAFE;
 
@@ -175,7 +186,8 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         const int kend = kend64 < g.K ? (int)kend64 : g.K;
         const bool to_ws = c0 > 0;
         int chunk = c0;
-        uint32_t mca = 0, mcb = 0;           // largest magnitude codes seen
+        float amax_a = 0.0f, amax_b = 0.0f;  // largest magnitudes decoded
+        uint32_t special = 0;                // Inf/NaN codes seen
 
         auto rnd = [&](float x) __attribute__((always_inline)) -> float {
             return SAFE ? rn16s(x) : rn16v(x);
@@ -237,8 +249,8 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         int crem = g.CL;                 // products left in the current chunk
         slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, kbeg, kend, tid, ra);
         slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, kbeg, kend, tid, rb);
-        slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[0][0][0], BM + PA, tid, ra, mca);
-        slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[0][0][0], BN + PB, tid, rb, mcb);
+        slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[0][0][0], BM + PA, tid, ra, amax_a, special);
+        slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[0][0][0], BN + PB, tid, rb, amax_b, special);
         __syncthreads();
         for (int s = 0; s < nslabs; ++s) {
             const int buf = s & 1;
@@ -285,28 +297,29 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                 }
             }
             if (s + 1 < nslabs) {
-                slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[buf ^ 1][0][0], BM + PA, tid, ra, mca);
-                slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[buf ^ 1][0][0], BN + PB, tid, rb, mcb);
+                slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[buf ^ 1][0][0], BM + PA, tid, ra, amax_a, special);
+                slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[buf ^ 1][0][0], BN + PB, tid, rb, amax_b, special);
             }
             __syncthreads();
         }
         if (crem != g.CL) flush();       // the last, shorter chunk
 
         if (!SAFE) {
-            // Largest codes over the workgroup's operands of this piece.  The
-            // bound uses the full K, so that pieces of one tile that each pass
-            // bound the whole chain together.
-            if (tid == 0) { s_mcode[0] = 0; s_mcode[1] = 0; }
+            // Largest magnitudes over the workgroup's operands of this piece.
+            // The bound uses the full K, so that pieces of one tile that each
+            // pass bound the whole chain together.
+            if (tid == 0) { s_track[0] = 0; s_track[1] = 0; s_track[2] = 0; }
             __syncthreads();
-            atomicMax(&s_mcode[0], mca);
-            atomicMax(&s_mcode[1], mcb);
+            atomicMax(&s_track[0], __float_as_uint(amax_a));   // non-negative: bit order
+            atomicMax(&s_track[1], __float_as_uint(amax_b));
+            atomicOr(&s_track[2], special);
             __syncthreads();
-            const uint32_t ca = s_mcode[0], cb = s_mcode[1];
-            __syncthreads();                 // s_mcode is reused by the next piece
-            if (ca >= 0x7Cu || cb >= 0x7Cu) return false;       // Inf or NaN operand
-            const double bound = 9.0 * (double)g.K * (double)fp8_to_f32<0>(ca) *
-                                 (double)fp8_to_f32<0>(cb);
-            if (!(bound < 2147483648.0)) return false;         // 2^31
+            const float ma = __uint_as_float(s_track[0]), mb = __uint_as_float(s_track[1]);
+            const uint32_t sp = s_track[2];
+            __syncthreads();                 // s_track is reused by the next piece
+            if (sp) return false;                                   // Inf or NaN operand
+            const double bound = 9.0 * (double)g.K * (double)ma * (double)mb;
+            if (!(bound < 2147483648.0)) return false;             // 2^31
         }
         if (to_ws) return true;
         // The running sum: a lane's TN consecutive codes of a row are stored

@@ -281,6 +281,26 @@ def test_chunk_gemm_degenerate():
             assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, mode=mode))
 
 
+@pytest.mark.parametrize("guard", ["1", "0"])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_chunk_gemm_decodes_every_code(ta, tb, guard, monkeypatch):
+    """All 256 FP8 codes (finite, subnormal, +-0, Inf, NaN) through both
+    operands: a selection-like partner (1, 0, -1) makes the outputs the
+    codes' own values and simple sums of them."""
+    monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+    codes = np.arange(256, dtype=np.uint8)
+    X = np.stack([codes, codes[::-1]], axis=1)                 # 256 x 2
+    Y = np.array([[0x3C, 0x00, 0xBC], [0x00, 0x3C, 0x3C]], np.uint8)   # 2 x 3
+    for A, B, M, N in ((X, Y, 256, 3), (Y.T.copy(), X.T.copy(), 3, 256)):
+        As = np.ascontiguousarray(A.T) if ta else A
+        Bs = np.ascontiguousarray(B.T) if tb else B
+        for CL in (1, 2):
+            say(f"decode every code ta={ta} tb={tb} guard={guard} M={M} N={N} CL={CL}")
+            Cg = host(gemm(dev(As), dev(Bs), M, N, 2, CL, ta, tb))
+            Co = oracle.chunk_gemm(As, Bs, CL, ta, tb)
+            assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
+
+
 def test_chunk_gemm_guard_falls_back_per_piece(monkeypatch):
     """Tiles whose operands could overflow (or hold Inf/NaN) fail the guarded
     path's check and are recomputed on the safe path, in the same launch as
