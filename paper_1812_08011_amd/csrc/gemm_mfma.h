@@ -1,0 +1,25 @@
+// Matrix-core chunk_gemm kernels of the fast mode (gemm_mfma.hip): tile
+// shapes and kernel entry addresses, for the host-side planner in
+// chunk_gemm.hip.
+#pragma once
+
+#include "gemm_plan.h"
+
+namespace fp8t {
+
+struct MfmaShape {
+    int BW;         // MFMA block (32: 32x32x16, 16: 16x16x32)
+    int BM, BN;     // outputs per workgroup
+    int NT;         // threads per workgroup
+    int kstep;      // products per instruction: CL must be a multiple
+};
+
+constexpr int kMfmaConfigs = 2;
+
+MfmaShape mfma_shape(int cfg);
+
+// __global__ function of configuration cfg (0 .. kMfmaConfigs-1) for the
+// given operand layouts, taking (GemmArgs, Plan).
+const void* mfma_kernel(int cfg, int ta, int tb);
+
+}  // namespace fp8t

@@ -43,7 +43,18 @@ struct Plan {
     int64_t L;          // tile-chunks shared out
     int nch;            // chunks per tile
     int G;              // workgroups
+    int xcd_remap;      // whole tiles are grouped by XCD (see whole_tile)
 };
+
+// Tile of whole-tile work item t.  Workgroups are dealt to the 8 XCDs of the
+// chip round-robin (workgroup w runs on XCD w % 8), and with G a multiple of 8
+// item t runs on XCD t % 8.  With xcd_remap, XCD x gets the contiguous range
+// of row-major tiles [x * t_whole / 8, (x + 1) * t_whole / 8): tiles that
+// share operand rows then share that XCD's L2.
+__host__ __device__ inline int64_t whole_tile(const Plan& p, int64_t t) {
+    if (!p.xcd_remap) return t;
+    return (t % 8) * (p.t_whole / 8) + t / 8;
+}
 
 // First chunk of shared tile lt that the workspace holds: the end of the
 // piece that starts at the tile's chunk 0 (nch if the tile is not split).

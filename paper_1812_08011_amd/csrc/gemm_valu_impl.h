@@ -357,7 +357,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         int64_t tile, lt;
         int c0, c1;
         if (t < p.t_whole) {
-            tile = t;
+            tile = whole_tile(p, t);
             lt = -1;
             c0 = 0;
             c1 = p.nch;

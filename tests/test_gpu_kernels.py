@@ -221,19 +221,51 @@ def test_chunk_gemm_workspace_contract():
         assert np.array_equal(host(C), Co)
 
 
+@pytest.mark.parametrize("mtile", ["auto", "0", "1"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
-def test_chunk_gemm_fast_within_tolerance(ta, tb):
+def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
+    """Fast mode against the fast oracle within the derived tolerance, for
+    every matrix-core tile; the guarded and safe epilogues give the same
+    bits."""
+    if mtile != "auto":
+        monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
     rng = np.random.default_rng(520 + 2 * ta + tb)
     for (M, N, K, CL) in SHAPES:
         A, B = _operands(rng, M, N, K, ta, tb)
-        say(f"chunk_gemm fast ta={ta} tb={tb} M={M} N={N} K={K} CL={CL}")
-        Cg = host(gemm(dev(A), dev(B), M, N, K, CL, ta, tb, mode=fp8t.FAST))
+        say(f"chunk_gemm fast mtile={mtile} ta={ta} tb={tb} M={M} N={N} K={K} CL={CL}")
+        Ad, Bd = dev(A), dev(B)
+        monkeypatch.setenv("FP8T_GEMM_GUARD", "1")
+        Cg = host(gemm(Ad, Bd, M, N, K, CL, ta, tb, mode=fp8t.FAST))
+        monkeypatch.setenv("FP8T_GEMM_GUARD", "0")
+        Cs = host(gemm(Ad, Bd, M, N, K, CL, ta, tb, mode=fp8t.FAST))
+        assert np.array_equal(Cg, Cs), (M, N, K, CL, np.argwhere(Cg != Cs)[:5])
         Co = oracle.chunk_gemm(A, B, CL, ta, tb, mode=oracle.FAST)
         va = oracle.p8_value(A.T if ta else A)
         vb = oracle.p8_value(B.T if tb else B)
         check_fast(Cg, Co, abs_dot(va, vb), K, CL, f"fast {M}x{N}x{K} CL={CL}")
         if CL == 1:
             assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, ta, tb))
+
+
+@pytest.mark.parametrize("mtile", ["0", "1"])
+@pytest.mark.parametrize("wgs", ["2", "9"])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (1, 0), (0, 1)])
+def test_chunk_gemm_fast_shared_tiles(mtile, wgs, ta, tb, monkeypatch):
+    """Fast mode with tiles shared out over few workgroups (chunk sums through
+    the workspace and the fold pass) gives the bits of the whole-tile plan."""
+    monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
+    rng = np.random.default_rng(580 + 2 * ta + tb)
+    for (M, N, K, CL) in [(130, 67, 1000, 64), (64, 96, 4096, 32), (33, 47, 700, 32)]:
+        A, B = _operands(rng, M, N, K, ta, tb)
+        Ad, Bd = dev(A), dev(B)
+        monkeypatch.setenv("FP8T_GEMM_SPLIT", "0")
+        monkeypatch.delenv("FP8T_GEMM_WGS", raising=False)
+        say(f"fast shared mtile={mtile} wgs={wgs} ta={ta} tb={tb} {M}x{N}x{K} CL={CL}")
+        Cw = host(gemm(Ad, Bd, M, N, K, CL, ta, tb, mode=fp8t.FAST))
+        monkeypatch.setenv("FP8T_GEMM_SPLIT", "1")
+        monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
+        Cs = host(gemm(Ad, Bd, M, N, K, CL, ta, tb, mode=fp8t.FAST))
+        assert np.array_equal(Cw, Cs), (M, N, K, CL, np.argwhere(Cw != Cs)[:5])
 
 
 def test_chunk_gemm_padded_leading_dims_and_misaligned_bases():
@@ -321,14 +353,16 @@ def test_chunk_gemm_guard_falls_back_per_piece(monkeypatch):
             assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
 
 
-def test_chunk_gemm_overflow_to_inf():
+@pytest.mark.parametrize("guard", ["1", "0"])
+def test_chunk_gemm_overflow_to_inf(guard, monkeypatch):
     """Sums beyond the largest FP16 value become Inf and stay Inf."""
+    monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
     K = 64 * 40
     A = np.full((2, K), 0x7B, np.uint8)          # 57344
     B = np.full((K, 2), 0x7B, np.uint8)
     B[::2, 1] = 0xFB                              # alternate signs in column 1
     for mode in (fp8t.EXACT, fp8t.FAST):
-        say(f"chunk_gemm overflow mode={mode}")
+        say(f"chunk_gemm overflow mode={mode} guard={guard}")
         Cg = host(gemm(dev(A), dev(B), 2, 2, K, 64, mode=mode))
         Co = oracle.chunk_gemm(A, B, 64, mode=mode)
         assert np.array_equal(Cg, Co)
