@@ -43,6 +43,29 @@ HBM_BYTES_S = 8.0e12
 FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 
 
+# HBM traffic of the exact-mode chunk_gemm calls of one step, from two
+# rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) over this benchmark,
+# calibrated by the counters of a plain device copy of known size (fetch x2.0,
+# write x1.0); average calibrated bytes per call (forward 197.6 MB,
+# backward-data 257.4 MB, weight-gradient 3072.9 MB including the chunk sums
+# of its shared tiles and the fold pass).  Valid only for the kernel sources
+# they were measured on: any change to them reports null.
+TRAFFIC_SOURCES_SHA256 = "a2b7657ff4af5cbbbcd37b6d1285c6d4d4b6a9dcbe73b3b18ec9ece79bd2ddb5"
+EXACT_TRAFFIC_BYTES_PER_CALL = (197.6e6 + 257.4e6 + 3072.9e6) / 3
+
+
+def kernel_sources_sha256():
+    import hashlib
+    d = os.path.join(ROOT, "paper_1812_08011_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
 def exact_peak_mac_s(cl):
     """Emulation ceiling of one exact-mode multiply-accumulate: gfx950 has no
     adder for the paper's FP16, so a MAC costs at least one FP32 FMA plus
@@ -215,13 +238,16 @@ def main():
             "parallelism": "single GPU",
         },
         "roofline": {
-            "kernel": "chunk_gemm exact",
+            "kernel": "chunk_gemm exact mode (VALU kernel + fold pass), mean of the "
+                      "forward, backward-data and weight-gradient calls",
             "bound": "alu",
             "achieved": exact_achieved / 1e12,
             "peak": peak / 1e12,
             "unit": "TMAC/s",
             "frac": exact_achieved / peak,
-            "traffic": None,
+            "traffic": (EXACT_TRAFFIC_BYTES_PER_CALL
+                        if kernel_sources_sha256() == TRAFFIC_SOURCES_SHA256 else None),
+            "traffic_unit": "bytes per call",
         },
         "kernels": {
             "exact_gemm_gmac_s": 3 * gemm_macs / exact_s / 1e9,
