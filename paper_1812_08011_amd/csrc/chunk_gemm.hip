@@ -27,35 +27,63 @@ namespace {
 // fold: finish the shared tiles
 // ---------------------------------------------------------------------------
 
-// One thread per output of a shared tile: continue the running sum held in C
-// (the FP16 sum of the tile's first piece) over the chunk sums the other
-// pieces left in the workspace, in ascending chunk order -- the same
-// additions a whole-tile pass makes after its first piece.
+// FP16 code -> value * 2^96 without branches (the fold pass decodes one code
+// per output per chunk): normal, Inf and NaN codes map by placing the code's
+// exponent and significand in the FP32 fields; zero and subnormals (m 2^-39)
+// convert the significand.
+__device__ __forceinline__ float fp16_to_f32s_fold(uint32_t c) {
+    const uint32_t mag = c & 0x7FFFu;
+    const float fn = __uint_as_float((mag << 14) + (192u << 23));
+    const float fs = (float)(c & 0x1FFu) * 0x1p57f;
+    const float f = mag >= 0x200u ? fn : fs;
+    return __uint_as_float(__float_as_uint(f) | ((c & 0x8000u) << 16));
+}
+
+// Each thread takes kFoldV consecutive outputs of one row of a shared tile and
+// continues their running sums, held in C (the FP16 sums of the tile's first
+// piece), over the chunk sums the other pieces left in the workspace, in
+// ascending chunk order -- the same additions a whole-tile pass makes after
+// its first piece.  The chunk sums of kFoldV outputs are one 16-byte load per
+// chunk, issued kFoldU chunks ahead.
+constexpr int kFoldV = 8, kFoldU = 4;
+
 __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, int BN) {
     const int64_t per = (int64_t)BM * BN;
-    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t idx = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kFoldV;
     const int64_t lt = idx / per;
     if (lt * p.nch >= p.L) return;
     const int local = (int)(idx - lt * per);
     const int64_t tile = p.t_whole + lt;
     const int m = (int)(tile / p.tiles_n) * BM + local / BN;
-    const int n = (int)(tile % p.tiles_n) * BN + local % BN;
-    if (m >= g.M || n >= g.N) return;
+    const int n0 = (int)(tile % p.tiles_n) * BN + local % BN;
+    if (m >= g.M || n0 >= g.N) return;
     const int a = first_piece_end(p, lt);
     if (a >= p.nch) return;
-    uint16_t* cp = g.C + (int64_t)m * g.ldc + n;
-    float S = fp16_to_f32s(*cp);
-    const uint16_t* src = g.ws + lt * p.nch * per + local;
+    uint16_t* cp = g.C + (int64_t)m * g.ldc + n0;
+    const int nv = min(kFoldV, g.N - n0);
+    float S[kFoldV];
+#pragma unroll
+    for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fp16_to_f32s_fold(cp[v]) : 0.0f;
+    const uint4* src = reinterpret_cast<const uint4*>(g.ws + lt * p.nch * per + local);
+    const int64_t step = per / kFoldV;          // uint4 elements per chunk
+    auto add = [&](uint4 q) __attribute__((always_inline)) {
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int v = 0; v < kFoldV; ++v)
+            S[v] = rn16s(S[v] + fp16_to_f32s_fold((w[v / 2] >> (16 * (v % 2))) & 0xFFFFu));
+    };
     int c = a;
-    for (; c + 8 <= p.nch; c += 8) {
-        uint32_t v[8];
+    for (; c + kFoldU <= p.nch; c += kFoldU) {
+        uint4 q[kFoldU];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = src[(int64_t)(c + j) * per];
+        for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)(c + u) * step];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) S = rn16s(S + fp16_to_f32s(v[j]));
+        for (int u = 0; u < kFoldU; ++u) add(q[u]);
     }
-    for (; c < p.nch; ++c) S = rn16s(S + fp16_to_f32s(src[(int64_t)c * per]));
-    *cp = f32s_to_fp16(S);
+    for (; c < p.nch; ++c) add(src[(int64_t)c * step]);
+#pragma unroll
+    for (int v = 0; v < kFoldV; ++v)
+        if (v < nv) cp[v] = f32s_to_fp16(S[v]);
 }
 
 __global__ void fill_zero_u16(uint16_t* __restrict__ C, int M, int N, int64_t ldc) {
@@ -70,7 +98,7 @@ __global__ void fill_zero_u16(uint16_t* __restrict__ C, int M, int N, int64_t ld
 
 constexpr double kClockHz = 2.4e9;      // MI355X peak engine clock
 constexpr double kLanesPerCU = 128.0;   // 32-bit VALU lane-ops per clock per CU
-constexpr double kFoldBytesPerS = 4e12; // effective HBM rate of the fold pass
+constexpr double kFoldBytesPerS = 5e12; // effective HBM rate of the fold pass
 
 int env_int(const char* name, int dflt) {
     const char* v = getenv(name);
@@ -127,15 +155,15 @@ double valu_ops_per_mac(int cfg) {
     }
 }
 
-// Matrix-core fast mode: CU time of one output's chunk -- the VALU epilogue
-// (9 instructions) plus the part of the MFMA time it does not hide, and the
-// operand traffic per output that shrinks with the tile.
-double mfma_cost_per_output_chunk(const MfmaShape& sh, int64_t CL) {
-    const double valu = 10.0 / (kLanesPerCU * kClockHz);
-    const double mfma = 0.5 * (double)CL / 4.9e12;           // ~1.25 PMAC/s over 256 CUs
-    const double load = (double)CL * (1.0 / sh.BM + 1.0 / sh.BN) / 40e9;   // L2 bytes per CU
-    return valu + mfma + load;
+// Matrix-core fast mode, CU time of one output-chunk (the VALU epilogue
+// dominates; the matrix-core share grows with CL) and of the per-tile start
+// (pipeline fill, C stores), measured on the conv-stage GEMMs: 64 x 64 tiles
+// with 64-k slabs, 32 x 32 tiles with 128-k slabs.
+double mfma_cost_per_output_chunk(int cfg, int64_t CL) {
+    const double base = cfg == 0 ? 0.156e-9 : 0.17e-9;
+    return base * (0.6 + 0.4 * (double)CL / 64.0);
 }
+double mfma_cost_per_tile(int cfg) { return cfg == 0 ? 1.1e-6 : 0.66e-6; }
 
 enum Kind { VALU_EXACT = 0, VALU_FAST = 1, MFMA_FAST = 2 };
 
@@ -175,12 +203,14 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
             const void* fn;
             int NT, BM, BN;
             double t_out;                        // CU time of one output-chunk
+            double t_tile = 0.0;                 // CU time of a tile's start
             if (mf) {
                 const MfmaShape sh = mfma_shape(cfg);
                 if (CL % sh.kstep != 0) continue;
                 fn = mfma_kernel(cfg, ta, tb);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
-                t_out = mfma_cost_per_output_chunk(sh, CL);
+                t_out = mfma_cost_per_output_chunk(cfg, CL);
+                t_tile = mfma_cost_per_tile(cfg);
             } else {
                 const ValuShape sh = valu_shape(cfg);
                 fn = valu_kernel(cfg, ta, tb, fast);
@@ -191,9 +221,6 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
             int occ = kernel_occupancy(fn, NT);
             if (occ <= 0) continue;
             if (occ > 8) occ = 8;
-            // the matrix-core kernel alternates MFMA chains, epilogues and
-            // barriers within a wave: one wave per SIMD leaves it idle
-            if (mf && occ < 2) t_out *= 2.0;
             const int64_t tiles_m = (M + BM - 1) / BM;
             const int64_t tiles_n = (N + BN - 1) / BN;
             const int64_t T = tiles_m * tiles_n;
@@ -213,9 +240,9 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                     p.G = (int)G;
                     p.t_whole = T;
                     p.L = 0;
-                    // tile-chunks on the busiest CU
+                    // tiles on the busiest CU
                     const int64_t per_cu = (T + cus - 1) / cus;
-                    est = (double)per_cu * nch * t_chunk;
+                    est = (double)per_cu * (nch * t_chunk + t_tile);
                 } else {
                     int64_t G = gmax;
                     if (G > T * nch) G = T * nch;
@@ -227,7 +254,7 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                     const int64_t wg_per_cu = (G + cus - 1) / cus;
                     const int64_t per_wg = q * nch + (p.L + G - 1) / G;
                     ws = (size_t)(T - p.t_whole) * nch * BM * BN * sizeof(uint16_t) + kWsAlign;
-                    est = (double)wg_per_cu * per_wg * t_chunk +
+                    est = (double)wg_per_cu * (per_wg * t_chunk + (q + 2) * t_tile) +
                           2.0 * (double)ws / kFoldBytesPerS + 4e-6;
                 }
                 p.xcd_remap = p.t_whole % 8 == 0 && p.G % 8 == 0;
@@ -258,7 +285,7 @@ int launch_plan(const Choice& ch, GemmArgs g, hipStream_t stream) {
         return FP8T_EHIP;
     if (ch.plan.L > 0) {
         const int64_t shared = ch.plan.L / ch.plan.nch;
-        const int64_t threads = shared * ch.BM * ch.BN;
+        const int64_t threads = shared * ch.BM * ch.BN / kFoldV;
         hipLaunchKernelGGL(chunk_fold, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
                            stream, g, ch.plan, ch.BM, ch.BN);
     }

@@ -12,6 +12,7 @@ struct MfmaShape {
     int BM, BN;     // outputs per workgroup
     int NT;         // threads per workgroup
     int kstep;      // products per instruction: CL must be a multiple
+    int BK;         // k per LDS slab
 };
 
 constexpr int kMfmaConfigs = 2;

@@ -38,8 +38,6 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int kNT = 256;            // threads per workgroup
-constexpr int kBK = 64;             // k per LDS slab
-constexpr int kPitch = kBK + 8;     // bytes per LDS row (k-contiguous)
 
 // The 4 bytes (r, c .. c+3) of a row-major byte matrix with `rows` x `cols`
 // valid elements and leading dimension ld; bytes outside are 0.
@@ -71,8 +69,9 @@ __device__ __forceinline__ void transpose4x4(uint32_t d[4]) {
 // KC: k is contiguous in memory (element (r, k) at p[r * ld + k]) -- R x 16
 // words; otherwise the row index is (element at p[k * ld + r]) -- (R/4) x 16
 // blocks of 4 x 4 bytes, transposed in registers.
-template <bool KC, int R>
+template <bool KC, int R, int kBK>
 struct Slab {
+    static constexpr int kPitch = kBK + 8;     // bytes per LDS row (k-contiguous)
     static constexpr int U = KC ? R * (kBK / 4) : (R / 4) * (kBK / 4);
     static constexpr int PER = (U + kNT - 1) / kNT;
     static constexpr int NW = KC ? PER : 4 * PER;
@@ -166,8 +165,9 @@ template <> struct Mfma<16> {
     }
 };
 
-template <int BW, int FM, int FN, int kStages, bool TA, bool TB>
+template <int BW, int FM, int FN, int kStages, int kBK, bool TA, bool TB>
 __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
+    constexpr int kPitch = kBK + 8;     // bytes per LDS row (k-contiguous)
     using I = Mfma<BW>;
     constexpr int BM = 2 * FM * BW, BN = 2 * FN * BW;
     constexpr int KI = I::KI, NR = I::NR;
@@ -180,8 +180,8 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
     const int lane = tid & 63, wave = tid >> 6;
     const int wy = wave >> 1, wx = wave & 1;
 
-    Slab<!TA, BM> la[kStages];      // A is k-contiguous unless transposed
-    Slab<TB, BN> lb[kStages];       // B is k-contiguous only when transposed
+    Slab<!TA, BM, kBK> la[kStages];      // A is k-contiguous unless transposed
+    Slab<TB, BN, kBK> lb[kStages];       // B is k-contiguous only when transposed
 
     acc_t acc[FM][FN];
     float S[FM][FN][NR];
@@ -318,6 +318,18 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                         flush();
                         crem = g.CL;
                     }
+                } else if (kBK % 64 == 0 && kBK > 64 && g.CL == 64 && ks + kBK <= kend) {
+                    // the paper's chunk length, several chunks per full slab
+                    // (slabs start on chunk boundaries)
+#pragma unroll
+                    for (int q = 0; q < kBK / 64; ++q) {
+                        long a[64 / KI][FM], b[64 / KI][FN];
+#pragma unroll
+                        for (int st = 0; st < 64 / KI; ++st) read(a[st], b[st], q * (64 / KI) + st);
+#pragma unroll
+                        for (int st = 0; st < 64 / KI; ++st) mma(a[st], b[st]);
+                        flush();
+                    }
                 } else {
                     const int nsteps = (min(kBK, kend - ks) + KI - 1) / KI;
                     for (int st = 0; st < nsteps; ++st) {
@@ -382,27 +394,27 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
     }
 }
 
-template <int BW, int FM, int FN, int ST>
+template <int BW, int FM, int FN, int ST, int BK>
 const void* kernel_sel(int ta, int tb) {
-    if (!ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, false, false>);
-    if (!ta && tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, false, true>);
-    if (ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, true, false>);
-    return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, true, true>);
+    if (!ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, BK, false, false>);
+    if (!ta && tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, BK, false, true>);
+    if (ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, BK, true, false>);
+    return reinterpret_cast<const void*>(&chunk_gemm_mfma<BW, FM, FN, ST, BK, true, true>);
 }
 
 }  // namespace
 
 MfmaShape mfma_shape(int cfg) {
     switch (cfg) {
-        case 0: return MfmaShape{32, 64, 64, kNT, 16};
-        default: return MfmaShape{16, 32, 32, kNT, 32};
+        case 0: return MfmaShape{32, 64, 64, kNT, 16, 64};
+        default: return MfmaShape{16, 32, 32, kNT, 32, 128};
     }
 }
 
 const void* mfma_kernel(int cfg, int ta, int tb) {
     switch (cfg) {
-        case 0: return kernel_sel<32, 1, 1, 2>(ta, tb);
-        case 1: return kernel_sel<16, 1, 1, 2>(ta, tb);
+        case 0: return kernel_sel<32, 1, 1, 2, 64>(ta, tb);
+        case 1: return kernel_sel<16, 1, 1, 2, 128>(ta, tb);
         default: return nullptr;
     }
 }
