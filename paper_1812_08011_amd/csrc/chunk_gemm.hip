@@ -365,8 +365,10 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
     g.N = n;
     g.K = k;
     g.CL = cl;
-    g.a_vec = aligned(A, 4) && lda % 4 == 0;
-    g.b_vec = aligned(B, 4) && ldb % 4 == 0;
+    // 4-byte loads need aligned rows; the matrix-core kernel's interior path
+    // also keeps per-thread offsets within a slab in 32 bits
+    g.a_vec = aligned(A, 4) && lda % 4 == 0 && lda < (1 << 24);
+    g.b_vec = aligned(B, 4) && ldb % 4 == 0 && ldb < (1 << 24);
     g.c_vec = aligned(C, 4) && ldc % 2 == 0;
     // FP8T_GEMM_GUARD=0 runs every piece on the safe path (tests, tuning).
     g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;

@@ -96,23 +96,33 @@ struct Slab {
     }
 
     // The same when the whole slab lies inside the matrix and 4-byte loads
-    // are aligned: no bounds checks.
-    __device__ __forceinline__ void load_fast(const uint8_t* __restrict__ p, int64_t ld,
-                                              int row0, int k0, int tid) {
+    // are aligned: no bounds checks, and the addresses are one uniform base
+    // (the slab's first byte) plus per-thread 32-bit offsets fixed for the
+    // whole kernel, so the loads take the scalar-base form with no per-slab
+    // address arithmetic.
+    __device__ __forceinline__ static void offsets(int64_t ld, int tid, uint32_t (&o)[NW]) {
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int u = min(tid + kNT * q, U - 1);
+            if (KC) {
+                const int rr = u / (kBK / 4), kq = (u % (kBK / 4)) * 4;
+                o[q] = (uint32_t)(rr * ld + kq);
+            } else {
+                const int rg = u % (R / 4), kg = u / (R / 4);
+#pragma unroll
+                for (int b = 0; b < 4; ++b) o[q * 4 + b] = (uint32_t)((kg * 4 + b) * ld + rg * 4);
+            }
+        }
+    }
+    __device__ __forceinline__ void load_fast(const uint8_t* __restrict__ base, const uint32_t (&o)[NW],
+                                              int tid) {
 #pragma unroll
         for (int q = 0; q < PER; ++q) {
             const int u = tid + kNT * q;
             if (U % kNT != 0 && u >= U) continue;
-            if (KC) {
-                const int rr = u / (kBK / 4), kq = (u % (kBK / 4)) * 4;
-                r[q] = *reinterpret_cast<const uint32_t*>(p + (int64_t)(row0 + rr) * ld + k0 + kq);
-            } else {
-                const int rg = u % (R / 4), kg = u / (R / 4);
 #pragma unroll
-                for (int b = 0; b < 4; ++b)
-                    r[q * 4 + b] = *reinterpret_cast<const uint32_t*>(
-                        p + (int64_t)(k0 + kg * 4 + b) * ld + row0 + rg * 4);
-            }
+            for (int b = 0; b < (KC ? 1 : 4); ++b)
+                r[q * (KC ? 1 : 4) + b] = *reinterpret_cast<const uint32_t*>(base + o[q * (KC ? 1 : 4) + b]);
         }
     }
 
@@ -185,6 +195,12 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
 
     acc_t acc[FM][FN];
     float S[FM][FN][NR];
+    // per-thread offsets of the interior load path (see Slab::load_fast)
+    typedef Slab<!TA, BM, kBK> SlabA;
+    typedef Slab<TB, BN, kBK> SlabB;
+    uint32_t offa[SlabA::NW], offb[SlabB::NW];
+    SlabA::offsets(g.lda, tid, offa);
+    SlabB::offsets(g.ldb, tid, offb);
 
     auto piece = [&](auto safe_tag, int64_t tile, int c0, int c1, int64_t lt)
                      __attribute__((always_inline)) -> bool {
@@ -208,7 +224,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
 
         // chunk end: round each chunk sum, add it into S (or, for a piece
         // that does not start the tile, store it for the fold pass)
-        auto flush_sum = [&]() __attribute__((always_inline)) {
+        auto flush_sum = [&](acc_t (&acc)[FM][FN]) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -227,7 +243,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                         acc[i][j][r] = 0.0f;
                     }
         };
-        auto flush_ws = [&]() __attribute__((always_inline)) {
+        auto flush_ws = [&](acc_t (&acc)[FM][FN]) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -250,8 +266,8 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                 }
         };
         auto flush = [&]() __attribute__((always_inline)) {
-            if (to_ws) flush_ws();
-            else flush_sum();
+            if (to_ws) flush_ws(acc);
+            else flush_sum(acc);
             ++chunk;
         };
 
@@ -267,8 +283,10 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
         const bool slab_chunks = g.CL % kBK == 0;
         auto issue = [&](int u, int kk) __attribute__((always_inline)) {
             if (interior && kk + kBK <= kend) {
-                la[u].load_fast(g.A, g.lda, m0, kk, tid);
-                lb[u].load_fast(g.B, g.ldb, n0, kk, tid);
+                const uint8_t* ba = TA ? g.A + (int64_t)kk * g.lda + m0 : g.A + (int64_t)m0 * g.lda + kk;
+                const uint8_t* bb = TB ? g.B + (int64_t)n0 * g.ldb + kk : g.B + (int64_t)kk * g.ldb + n0;
+                la[u].load_fast(ba, offa, tid);
+                lb[u].load_fast(bb, offb, tid);
             } else {
                 la[u].load(g.A, g.lda, m0, kk, g.M, kend, g.a_vec, tid);
                 lb[u].load(g.B, g.ldb, n0, kk, g.N, kend, g.b_vec, tid);

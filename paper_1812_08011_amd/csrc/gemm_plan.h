@@ -31,8 +31,8 @@ struct GemmArgs {
     uint16_t* ws;       // chunk sums of the shared tiles (null when L == 0)
     int64_t lda, ldb, ldc;
     int M, N, K, CL;
-    int a_vec;          // A, lda allow 4-byte loads
-    int b_vec;          // B, ldb allow 4-byte loads
+    int a_vec;          // A, lda allow 4-byte loads (and lda < 2^24)
+    int b_vec;          // B, ldb allow 4-byte loads (and ldb < 2^24)
     int c_vec;          // C, ldc allow stores of a lane's whole row of codes
     int guarded;        // exact mode: try the guarded path first
 };
