@@ -105,12 +105,17 @@ int fp16_quantize(const float* src, uint16_t* dst, int64_t n,
  * Forward Y = X W: (0, 0).  Backward dX = dY W^T: trans_b = 1.
  * Gradient dW = X^T dY: trans_a = 1.
  * M, N, K >= 0; CL >= 1 (CL >= K means one chunk).  C must not overlap A or B.
- * workspace / workspace_bytes: device scratch of at least
- * chunk_gemm_workspace_size(...) bytes for the same arguments (may be NULL
- * when that size is 0); its contents on entry do not matter.
+ * workspace / workspace_bytes: optional device scratch, for the chunk sums
+ * of output tiles whose K range is shared out over several workgroups (the
+ * chunk sums are then added into the running sum in ascending order by a
+ * second pass, so the result is the same).  With workspace_bytes == 0 the
+ * call takes the fastest plan that needs none; otherwise workspace_bytes must
+ * be at least chunk_gemm_workspace_size(...) for the same arguments on the
+ * same device.  Its contents on entry do not matter.
  * Errors: FP8T_EINVAL (negative size, CL < 1, flag not 0/1, a leading
- * dimension too small, NULL pointer for a non-empty matrix);
- * FP8T_EWORKSPACE; FP8T_EHIP.
+ * dimension too small, NULL pointer for a non-empty matrix, NULL workspace
+ * with workspace_bytes > 0); FP8T_EWORKSPACE (0 < workspace_bytes < the
+ * query); FP8T_EHIP.
  */
 int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
@@ -118,11 +123,43 @@ int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
- * chunk_gemm_workspace_size -- bytes of workspace chunk_gemm needs for these
- * arguments (0 if none).  Returns 0 for invalid arguments as well.
+ * chunk_gemm_workspace_size -- bytes of workspace the fastest plan of
+ * chunk_gemm needs on the current device for these arguments (0 if none, or
+ * for invalid arguments, or when no device is present).
  */
 size_t chunk_gemm_workspace_size(int trans_a, int trans_b, int64_t M,
                                  int64_t N, int64_t K, int64_t CL, int mode);
+
+/*
+ * chunk_gemm_fp8 -- chunk_gemm with the result also rounded back to FP8 in
+ * the same pass (Sec. 2.1: the 16-bit sums of a GEMM "can then be rounded
+ * down to 8 bits" to feed the next layer's GEMMs), optionally scaled (e.g. by
+ * a loss scale, Sec. 3):
+ *
+ *   C8(i, j) = Q8(RN32(value(C(i, j)) * scale))
+ *
+ * with C(i, j) exactly as chunk_gemm computes it (same modes, layouts and
+ * rounding); Q8 and the FP32 product are those of fp8_quantize, so C8 equals
+ * fp8_quantize(C, FP8T_SRC_FP16, scale).  C (ldc >= N) may be NULL when only
+ * the FP8 result is wanted, which saves its 2 M N bytes of stores; C8 is
+ * M x N uint8_t row-major with ldc8 >= N and must not overlap A, B or C.
+ * workspace: at least chunk_gemm_fp8_workspace_size(...) bytes for the
+ * fastest plan, or none (then a plan that needs none; same results).
+ * Errors: as chunk_gemm, and FP8T_EINVAL for a NULL C8 or ldc8 < N.
+ */
+int chunk_gemm_fp8(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                   int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+                   int64_t ldb, uint16_t* C, int64_t ldc, uint8_t* C8,
+                   int64_t ldc8, float scale, int mode, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * chunk_gemm_fp8_workspace_size -- bytes of workspace the fastest plan of
+ * chunk_gemm_fp8 needs on the current device for these arguments (0 if
+ * none, or for invalid arguments).
+ */
+size_t chunk_gemm_fp8_workspace_size(int trans_a, int trans_b, int64_t M,
+                                     int64_t N, int64_t K, int64_t CL, int mode);
 
 /*
  * sr_weight_update -- one SGD step entirely in FP16 with floating-point

@@ -45,6 +45,11 @@ def lib():
                                  i32, vp, sz, vp]
         L.chunk_gemm_workspace_size.restype = sz
         L.chunk_gemm_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64, i32]
+        L.chunk_gemm_fp8.restype = i32
+        L.chunk_gemm_fp8.argtypes = [i32, i32, i64, i64, i64, i64, vp, i64, vp, i64, vp, i64,
+                                     vp, i64, f32, i32, vp, sz, vp]
+        L.chunk_gemm_fp8_workspace_size.restype = sz
+        L.chunk_gemm_fp8_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64, i32]
         L.sr_weight_update.restype = i32
         L.sr_weight_update.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, u64, u64, vp]
         L.fp8t_status_string.restype = ctypes.c_char_p
@@ -123,6 +128,23 @@ def chunk_gemm(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, mode=EXACT
                                           _ptr(C), int(ldc), int(mode), _ptr(workspace),
                                           int(workspace_bytes), _stream(stream)))
     return C
+
+
+def chunk_gemm_fp8_workspace_size(trans_a, trans_b, M, N, K, CL, mode):
+    return int(lib().chunk_gemm_fp8_workspace_size(int(trans_a), int(trans_b), int(M), int(N),
+                                                   int(K), int(CL), int(mode)))
+
+
+def chunk_gemm_fp8(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, C8, ldc8, scale=1.0,
+                   mode=EXACT, workspace=None, workspace_bytes=0, stream=None):
+    """The C-ABI call with the same argument order; C may be None (FP8 result
+    only)."""
+    _check("chunk_gemm_fp8",
+           lib().chunk_gemm_fp8(int(trans_a), int(trans_b), int(M), int(N), int(K), int(CL),
+                                _ptr(A), int(lda), _ptr(B), int(ldb), _ptr(C), int(ldc), _ptr(C8),
+                                int(ldc8), float(scale), int(mode), _ptr(workspace),
+                                int(workspace_bytes), _stream(stream)))
+    return C8
 
 
 def sr_weight_update(w, g, v, w8, n, lr, momentum, weight_decay, seed, offset, stream=None):

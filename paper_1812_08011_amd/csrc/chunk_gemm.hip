@@ -58,12 +58,15 @@ __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, in
     const int n0 = (int)(tile % p.tiles_n) * BN + local % BN;
     if (m >= g.M || n0 >= g.N) return;
     const int a = first_piece_end(p, lt);
-    if (a >= p.nch) return;
-    uint16_t* cp = g.C + (int64_t)m * g.ldc + n0;
+    // a tile whose first piece took every chunk needs only its FP8 result
+    if (a >= p.nch && !g.C8) return;
+    // the running sum of the first piece: in C, or in s_ws (FP8 result only)
+    uint16_t* cp = g.C ? g.C + (int64_t)m * g.ldc + n0 : nullptr;
+    const uint16_t* sp = g.C ? cp : g.s_ws + lt * per + local;
     const int nv = min(kFoldV, g.N - n0);
     float S[kFoldV];
 #pragma unroll
-    for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fp16_to_f32s_fold(cp[v]) : 0.0f;
+    for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fp16_to_f32s_fold(sp[v]) : 0.0f;
     const uint4* src = reinterpret_cast<const uint4*>(g.ws + lt * p.nch * per + local);
     const int64_t step = per / kFoldV;          // uint4 elements per chunk
     auto add = [&](uint4 q) __attribute__((always_inline)) {
@@ -82,14 +85,22 @@ __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, in
     }
     for (; c < p.nch; ++c) add(src[(int64_t)c * step]);
 #pragma unroll
-    for (int v = 0; v < kFoldV; ++v)
-        if (v < nv) cp[v] = f32s_to_fp16(S[v]);
+    for (int v = 0; v < kFoldV; ++v) {
+        if (v >= nv) continue;
+        if (cp) cp[v] = f32s_to_fp16(S[v]);
+        if (g.C8) g.C8[(int64_t)m * g.ldc8 + n0 + v] = (uint8_t)f32d_to_fp8_scaled<96>(S[v], g.q_scale);
+    }
 }
 
-__global__ void fill_zero_u16(uint16_t* __restrict__ C, int M, int N, int64_t ldc) {
+// K = 0: every result is +0 (FP16 code 0, FP8 code of 0 * scale).
+__global__ void fill_empty(uint16_t* __restrict__ C, int64_t ldc, uint8_t* __restrict__ C8,
+                           int64_t ldc8, float scale, int M, int N) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t total = (int64_t)M * N;
-    if (i < total) C[(i / N) * ldc + (i % N)] = 0;
+    if (i >= total) return;
+    const int64_t r = i / N, c = i % N;
+    if (C) C[r * ldc + c] = 0;
+    if (C8) C8[r * ldc8 + c] = (uint8_t)f32_to_fp8(0.0f * scale);
 }
 
 // ---------------------------------------------------------------------------
@@ -312,24 +323,33 @@ Kind kind_of(int mode, int64_t K, int64_t CL) {
     if (mode == FP8T_EXACT) return VALU_EXACT;
     return cl % 16 == 0 ? MFMA_FAST : VALU_FAST;
 }
-}  // namespace
-
-extern "C" size_t chunk_gemm_workspace_size(int trans_a, int trans_b, int64_t M,
-                                            int64_t N, int64_t K, int64_t CL, int mode) {
-    if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, mode)) return 0;
-    if (M == 0 || N == 0 || K == 0) return 0;
-    const int64_t cl = CL > K ? K : CL;
-    const Choice ch = plan_gemm(kind_of(mode, K, cl), trans_a, trans_b, M, N, K, cl, true);
-    return ch.cfg < 0 ? 0 : ch.ws_bytes;
+// Workspace of a plan: the chunk sums of its shared tiles, and (entry points
+// with an FP8 result) room for their first pieces' running sums.
+size_t plan_workspace(const Choice& ch, bool fp8out) {
+    if (ch.cfg < 0 || ch.plan.L == 0) return 0;
+    size_t b = ch.ws_bytes;
+    if (fp8out)
+        b += (size_t)(ch.plan.L / ch.plan.nch) * ch.BM * ch.BN * sizeof(uint16_t) + kWsAlign;
+    return b;
 }
 
-extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
-                          int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
-                          int64_t ldb, uint16_t* C, int64_t ldc, int mode,
-                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+size_t workspace_query(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, int mode,
+                       bool fp8out) {
+    if (!gemm_args_ok(ta, tb, M, N, K, CL, mode)) return 0;
+    if (M == 0 || N == 0 || K == 0) return 0;
+    const int64_t cl = CL > K ? K : CL;
+    return plan_workspace(plan_gemm(kind_of(mode, K, cl), ta, tb, M, N, K, cl, true), fp8out);
+}
+
+int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t CL,
+              const uint8_t* A, int64_t lda, const uint8_t* B, int64_t ldb, uint16_t* C,
+              int64_t ldc, uint8_t* C8, int64_t ldc8, float scale, int mode, void* workspace,
+              size_t workspace_bytes, hipStream_t stream, bool fp8out) {
     if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, mode)) return FP8T_EINVAL;
     if (M == 0 || N == 0) return FP8T_OK;
-    if (!C || ldc < N) return FP8T_EINVAL;
+    if (!fp8out && !C) return FP8T_EINVAL;
+    if (C && ldc < N) return FP8T_EINVAL;
+    if (fp8out && (!C8 || ldc8 < N)) return FP8T_EINVAL;
     if (K > 0) {
         if (!A || !B) return FP8T_EINVAL;
         if (lda < (trans_a ? M : K) || ldb < (trans_b ? K : N)) return FP8T_EINVAL;
@@ -339,8 +359,8 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
     const int m = (int)M, n = (int)N, k = (int)K, cl = (int)(K > 0 ? CL : 1);
     if (K == 0) {
         const int64_t total = M * N;
-        hipLaunchKernelGGL(fill_zero_u16, dim3((unsigned)((total + 255) / 256)), dim3(256),
-                           0, stream, C, m, n, ldc);
+        hipLaunchKernelGGL(fill_empty, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                           stream, C, ldc, C8, ldc8, scale, m, n);
         return launch_status();
     }
     // With no workspace, the best plan that needs none; with one, the best
@@ -348,19 +368,24 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
     const Choice ch = plan_gemm(kind_of(mode, K, cl), trans_a, trans_b, M, N, K, cl,
                                 workspace_bytes > 0);
     if (ch.cfg < 0) return FP8T_EHIP;
-    if (ch.ws_bytes > workspace_bytes) return FP8T_EWORKSPACE;
+    if (plan_workspace(ch, fp8out) > workspace_bytes) return FP8T_EWORKSPACE;
     GemmArgs g{};
     g.A = A;
     g.B = B;
     g.C = C;
-    g.ws = nullptr;
+    g.C8 = C8;
+    g.ldc8 = ldc8;
+    g.q_scale = scale;
     if (ch.plan.L > 0) {
         const uintptr_t base = ((uintptr_t)workspace + kWsAlign - 1) & ~(uintptr_t)(kWsAlign - 1);
         g.ws = reinterpret_cast<uint16_t*>(base);
+        const uintptr_t sbase = (base + ch.ws_bytes - kWsAlign + kWsAlign - 1) &
+                                ~(uintptr_t)(kWsAlign - 1);
+        g.s_ws = fp8out ? reinterpret_cast<uint16_t*>(sbase) : nullptr;
     }
     g.lda = lda;
     g.ldb = ldb;
-    g.ldc = ldc;
+    g.ldc = C ? ldc : 0;
     g.M = m;
     g.N = n;
     g.K = k;
@@ -369,8 +394,36 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
     // also keeps per-thread offsets within a slab in 32 bits
     g.a_vec = aligned(A, 4) && lda % 4 == 0 && lda < (1 << 24);
     g.b_vec = aligned(B, 4) && ldb % 4 == 0 && ldb < (1 << 24);
-    g.c_vec = aligned(C, 4) && ldc % 2 == 0;
+    g.c_vec = C && aligned(C, 4) && ldc % 2 == 0;
     // FP8T_GEMM_GUARD=0 runs every piece on the safe path (tests, tuning).
     g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
     return launch_plan(ch, g, stream);
+}
+}  // namespace
+
+extern "C" size_t chunk_gemm_workspace_size(int trans_a, int trans_b, int64_t M,
+                                            int64_t N, int64_t K, int64_t CL, int mode) {
+    return workspace_query(trans_a, trans_b, M, N, K, CL, mode, false);
+}
+
+extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                          int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+                          int64_t ldb, uint16_t* C, int64_t ldc, int mode,
+                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return gemm_call(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, nullptr, 0, 1.0f,
+                     mode, workspace, workspace_bytes, stream, false);
+}
+
+extern "C" size_t chunk_gemm_fp8_workspace_size(int trans_a, int trans_b, int64_t M,
+                                                int64_t N, int64_t K, int64_t CL, int mode) {
+    return workspace_query(trans_a, trans_b, M, N, K, CL, mode, true);
+}
+
+extern "C" int chunk_gemm_fp8(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                              int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+                              int64_t ldb, uint16_t* C, int64_t ldc, uint8_t* C8,
+                              int64_t ldc8, float scale, int mode, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+    return gemm_call(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, C8, ldc8, scale,
+                     mode, workspace, workspace_bytes, stream, true);
 }

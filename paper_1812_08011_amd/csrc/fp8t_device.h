@@ -156,6 +156,14 @@ __device__ __forceinline__ uint32_t f32_to_fp8(float x) {
     return r | s;
 }
 
+// FP8 code of an FP16 result held as a float on the FP16 grid scaled by 2^S:
+// Q8(RN32(value * scale)), the same as quantizing the result's FP16 code.
+template <int S>
+__device__ __forceinline__ uint32_t f32d_to_fp8_scaled(float x, float scale) {
+    const float v = S ? x * __builtin_ldexpf(1.0f, -S) : x;     // exact
+    return f32_to_fp8(v * scale);
+}
+
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).
 struct u32x4 { uint32_t x, y, z, w; };
 

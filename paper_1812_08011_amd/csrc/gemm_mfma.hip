@@ -368,16 +368,29 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
 
         if (!SAFE && __syncthreads_or(!(vmax < 4294967296.0f))) return false;   // 2^32
         if (to_ws) return true;
+        // the first piece of a shared tile leaves its running sum for the
+        // fold pass (in C, or in s_ws when only the FP8 result is wanted);
+        // whole tiles write the results
+        const bool keep = lt >= 0 && !g.C;
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
             for (int j = 0; j < FN; ++j) {
-                const int n = n0 + wx * FN * BW + j * BW + I::out_col(lane);
-                if (n >= g.N) continue;
+                const int nt = wx * FN * BW + j * BW + I::out_col(lane);
+                const int n = n0 + nt;
 #pragma unroll
                 for (int r = 0; r < NR; ++r) {
-                    const int m = m0 + wy * FM * BW + i * BW + I::out_row(lane, r);
-                    if (m < g.M) g.C[(int64_t)m * g.ldc + n] = f32d_to_fp16<DOM>(S[i][j][r]);
+                    const int mt = wy * FM * BW + i * BW + I::out_row(lane, r);
+                    const int m = m0 + mt;
+                    if (keep) {
+                        g.s_ws[(lt * BM + mt) * BN + nt] = f32d_to_fp16<DOM>(S[i][j][r]);
+                        continue;
+                    }
+                    if (n >= g.N || m >= g.M) continue;
+                    if (g.C) g.C[(int64_t)m * g.ldc + n] = f32d_to_fp16<DOM>(S[i][j][r]);
+                    if (g.C8 && lt < 0)
+                        g.C8[(int64_t)m * g.ldc8 + n] =
+                            (uint8_t)f32d_to_fp8_scaled<DOM>(S[i][j][r], g.q_scale);
                 }
             }
         return true;

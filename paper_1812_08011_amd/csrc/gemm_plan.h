@@ -27,8 +27,12 @@ namespace fp8t {
 struct GemmArgs {
     const uint8_t* A;
     const uint8_t* B;
-    uint16_t* C;
+    uint16_t* C;        // FP16 result (may be null when C8 is set)
     uint16_t* ws;       // chunk sums of the shared tiles (null when L == 0)
+    uint16_t* s_ws;     // running sums of the shared tiles' first pieces when C is null
+    uint8_t* C8;        // FP8 result Q8(value * q_scale), or null
+    int64_t ldc8;
+    float q_scale;
     int64_t lda, ldb, ldc;
     int M, N, K, CL;
     int a_vec;          // A, lda allow 4-byte loads (and lda < 2^24)

@@ -322,25 +322,45 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             if (!(bound < 2147483648.0)) return false;             // 2^31
         }
         if (to_ws) return true;
+        // The first piece of a shared tile leaves its running sum for the
+        // fold pass: in C, or in s_ws when only the FP8 result is wanted.
+        if (lt >= 0 && !g.C) {
+            uint16_t* dst = g.s_ws + (lt * BM + ly * TM) * BN + lx * TN;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) dst[i * BN + j] = f32d_to_fp16<DOM>(S[i][j]);
+            return true;
+        }
         // The running sum: a lane's TN consecutive codes of a row are stored
-        // in pairs when the whole row lies inside C and is aligned.
+        // in pairs when the whole row lies inside C and is aligned; the FP8
+        // result (whole tiles only: shared tiles get it from the fold pass)
+        // byte by byte.
         const int nl = n0 + lx * TN;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             const int m = m0 + ly * TM + i;
             if (m >= g.M) continue;
-            uint16_t* crow = g.C + (int64_t)m * g.ldc + nl;
-            if (TN > 1 && g.c_vec && nl + TN <= g.N) {
+            if (g.C) {
+                uint16_t* crow = g.C + (int64_t)m * g.ldc + nl;
+                if (TN > 1 && g.c_vec && nl + TN <= g.N) {
 #pragma unroll
-                for (int j = 0; j < TN; j += 2) {
-                    uint32_t c = (uint32_t)f32d_to_fp16<DOM>(S[i][j]) |
-                                 ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 1]) << 16);
-                    reinterpret_cast<uint32_t*>(crow)[j / 2] = c;
+                    for (int j = 0; j < TN; j += 2) {
+                        uint32_t c = (uint32_t)f32d_to_fp16<DOM>(S[i][j]) |
+                                     ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 1]) << 16);
+                        reinterpret_cast<uint32_t*>(crow)[j / 2] = c;
+                    }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        if (nl + j < g.N) crow[j] = f32d_to_fp16<DOM>(S[i][j]);
                 }
-            } else {
+            }
+            if (g.C8 && lt < 0) {
+                uint8_t* qrow = g.C8 + (int64_t)m * g.ldc8 + nl;
 #pragma unroll
                 for (int j = 0; j < TN; ++j)
-                    if (nl + j < g.N) crow[j] = f32d_to_fp16<DOM>(S[i][j]);
+                    if (nl + j < g.N) qrow[j] = (uint8_t)f32d_to_fp8_scaled<DOM>(S[i][j], g.q_scale);
             }
         }
         return true;

@@ -33,6 +33,7 @@ def lib():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "fp8_quantize", "fp16_quantize", "chunk_gemm", "chunk_gemm_workspace_size",
+        "chunk_gemm_fp8", "chunk_gemm_fp8_workspace_size",
         "sr_weight_update", "fp8t_status_string"])
 
 
@@ -91,8 +92,38 @@ def test_chunk_gemm_rejects(lib):
     assert _gemm(lib, N=0, C=None) == fp8t.OK
 
 
-def test_workspace_size_is_zero_for_direct_kernels(lib):
+def _gemm8(lib, **kw):
+    a = dict(ta=0, tb=0, M=4, N=4, K=4, CL=2, A=FAKE, lda=4, B=FAKE, ldb=4, C=FAKE, ldc=4,
+             C8=FAKE, ldc8=4, scale=1.0, mode=0, ws=None, wsb=0)
+    a.update(kw)
+    return lib.chunk_gemm_fp8(a["ta"], a["tb"], a["M"], a["N"], a["K"], a["CL"], a["A"],
+                              a["lda"], a["B"], a["ldb"], a["C"], a["ldc"], a["C8"], a["ldc8"],
+                              a["scale"], a["mode"], a["ws"], a["wsb"], None)
+
+
+def test_chunk_gemm_fp8_rejects(lib):
+    E = fp8t.EINVAL
+    assert _gemm8(lib, C8=None) == E
+    assert _gemm8(lib, ldc8=3) == E
+    assert _gemm8(lib, ldc=3) == E                      # C given with ldc < N
+    assert _gemm8(lib, CL=0) == E
+    assert _gemm8(lib, mode=5) == E
+    assert _gemm8(lib, lda=3) == E
+    assert _gemm8(lib, A=None) == E
+    assert _gemm8(lib, ws=None, wsb=64) == E            # workspace size without a pointer
+    assert _gemm8(lib, M=0) == fp8t.OK
+    assert _gemm(lib, ws=None, wsb=64) == E
+
+
+def test_workspace_size_without_a_device(lib):
+    """The query plans for the current device; with none it reports 0, and 0
+    for invalid arguments."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a device is present")
     assert fp8t.chunk_gemm_workspace_size(0, 0, 128, 128, 1024, 64, 0) == 0
+    assert fp8t.chunk_gemm_fp8_workspace_size(0, 0, 128, 128, 1024, 64, 0) == 0
+    assert fp8t.chunk_gemm_workspace_size(0, 0, 128, 128, 1024, 0, 0) == 0
 
 
 def test_sr_weight_update_rejects(lib):
