@@ -125,6 +125,59 @@ def cpu_baseline(work, target_s):
                       f"backward and gradient GEMMs ({macs / 1e6:.0f} M MAC, {t:.1f} s)"}
 
 
+def time_ms(torch, fn, reps):
+    """Average milliseconds of fn() over reps calls, from HIP events on the
+    current stream (the one the library launches on), after one warm-up."""
+    fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
+    """Measured outside the timed step:
+    * the Backward-data GEMM (the step's largest result, 50176 x 2304) with its
+      FP16 result rounded back to FP8 in the same pass (chunk_gemm_fp8, FP8
+      result only) against chunk_gemm followed by fp8_quantize of the FP16
+      result, both modes;
+    * sr_weight_update at a 50-layer residual CNN's 25.6 M parameters
+      (momentum 0.9, weight decay 1e-4, FP8 copy), against HBM."""
+    out = {}
+    C16, C8 = u16(M, K), u8(M, K)
+    for mode, tag in ((fp8t.EXACT, "exact"), (fp8t.FAST, "fast")):
+        wb = fp8t.chunk_gemm_fp8_workspace_size(0, 1, M, K, N, CL, mode)
+        w16b = fp8t.chunk_gemm_workspace_size(0, 1, M, K, N, CL, mode)
+        ws8 = u8(wb) if wb else None
+        ws16 = u8(w16b) if w16b else None
+        fused = time_ms(torch, lambda: fp8t.chunk_gemm_fp8(0, 1, M, K, N, CL, D8, N, W8, N, None,
+                                                           K, C8, K, 1.0, mode, ws8, wb), 3)
+
+        def two_pass():
+            fp8t.chunk_gemm(0, 1, M, K, N, CL, D8, N, W8, N, C16, K, mode, ws16, w16b)
+            fp8t.fp8_quantize(C16, C8)
+        out[f"dgrad_fp8_out_{tag}_ms"] = {"fused": fused, "gemm_then_quantize": time_ms(torch, two_pass, 3)}
+    n = 25_600_000
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    w16, g16, v16, w8 = u16(n), u16(n), u16(n), u8(n)
+    fp8t.fp16_quantize(torch.randn(n, device="cuda", generator=g) * 0.02, w16)
+    fp8t.fp16_quantize(torch.randn(n, device="cuda", generator=g) * 1e-4, g16)
+    fp8t.fp16_quantize(torch.randn(n, device="cuda", generator=g) * 1e-4, v16)
+    step = [0]
+
+    def upd():
+        step[0] += 1
+        fp8t.sr_weight_update(w16, g16, v16, w8, n, 0.1, 0.9, 1e-4, 7, step[0])
+    t = time_ms(torch, upd, 20)
+    out["sr_update_25_6M"] = {"us": t * 1e3, "gb_s": 11 * n / (t * 1e-3) / 1e9,
+                              "frac_of_hbm": 11 * n / (t * 1e-3) / HBM_BYTES_S}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -262,6 +315,7 @@ def main():
             "quantize_gb_s": q_bytes / per["quantize"] / 1e9,
         },
     }
+    result["kernels"].update(extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16))
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(work, args.cpu_seconds)
     print(json.dumps(result), flush=True)

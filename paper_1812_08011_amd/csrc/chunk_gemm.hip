@@ -395,6 +395,8 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     g.a_vec = aligned(A, 4) && lda % 4 == 0 && lda < (1 << 24);
     g.b_vec = aligned(B, 4) && ldb % 4 == 0 && ldb < (1 << 24);
     g.c_vec = C && aligned(C, 4) && ldc % 2 == 0;
+    g.c_vec16 = C && aligned(C, 16) && ldc % 8 == 0;
+    g.c8_vec8 = C8 && aligned(C8, 8) && ldc8 % 8 == 0;
     // FP8T_GEMM_GUARD=0 runs every piece on the safe path (tests, tuning).
     g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
     return launch_plan(ch, g, stream);

@@ -368,31 +368,64 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
 
         if (!SAFE && __syncthreads_or(!(vmax < 4294967296.0f))) return false;   // 2^32
         if (to_ws) return true;
-        // the first piece of a shared tile leaves its running sum for the
-        // fold pass (in C, or in s_ws when only the FP8 result is wanted);
-        // whole tiles write the results
-        const bool keep = lt >= 0 && !g.C;
+        // Results leave through LDS (free after the last slab's barrier): the
+        // tile's FP16 codes are staged there, then every thread writes 8
+        // consecutive codes of a row -- 16-byte stores of C, 8-byte stores of
+        // the FP8 result.  The first piece of a shared tile leaves its running
+        // sum for the fold pass instead (in C, or in s_ws when only the FP8
+        // result is wanted); whole tiles write the results.
+        uint16_t* ot = reinterpret_cast<uint16_t*>(&As[0][0][0]);
+        static_assert(BM * BN * 2 <= (int)sizeof(As), "staging tile exceeds LDS slab");
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const int nt = wx * FN * BW + j * BW + I::out_col(lane);
-                const int n = n0 + nt;
+            for (int j = 0; j < FN; ++j)
 #pragma unroll
-                for (int r = 0; r < NR; ++r) {
-                    const int mt = wy * FM * BW + i * BW + I::out_row(lane, r);
-                    const int m = m0 + mt;
-                    if (keep) {
-                        g.s_ws[(lt * BM + mt) * BN + nt] = f32d_to_fp16<DOM>(S[i][j][r]);
-                        continue;
-                    }
-                    if (n >= g.N || m >= g.M) continue;
-                    if (g.C) g.C[(int64_t)m * g.ldc + n] = f32d_to_fp16<DOM>(S[i][j][r]);
-                    if (g.C8 && lt < 0)
-                        g.C8[(int64_t)m * g.ldc8 + n] =
-                            (uint8_t)f32d_to_fp8_scaled<DOM>(S[i][j][r], g.q_scale);
+                for (int r = 0; r < NR; ++r)
+                    ot[(wy * FM * BW + i * BW + I::out_row(lane, r)) * BN + wx * FN * BW +
+                       j * BW + I::out_col(lane)] = f32d_to_fp16<DOM>(S[i][j][r]);
+        __syncthreads();
+        const bool keep = lt >= 0 && !g.C;
+        for (int u = tid; u < BM * BN / 8; u += kNT) {
+            const int row = u / (BN / 8), col = (u % (BN / 8)) * 8;
+            const uint4 q = *reinterpret_cast<const uint4*>(&ot[row * BN + col]);
+            if (keep) {
+                *reinterpret_cast<uint4*>(g.s_ws + (lt * BM + row) * BN + col) = q;
+                continue;
+            }
+            const int m = m0 + row, n = n0 + col;
+            if (m >= g.M) continue;
+            const uint32_t cw[4] = {q.x, q.y, q.z, q.w};
+            if (g.C) {
+                uint16_t* cp = g.C + (int64_t)m * g.ldc + n;
+                if (g.c_vec16 && n + 8 <= g.N) {
+                    *reinterpret_cast<uint4*>(cp) = q;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (n + e < g.N) cp[e] = (uint16_t)(cw[e / 2] >> (16 * (e % 2)));
                 }
             }
+            if (g.C8 && lt < 0) {
+                uint32_t b8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    b8[e] = f32_to_fp8(fp16_to_f32((cw[e / 2] >> (16 * (e % 2))) & 0xFFFFu) *
+                                       g.q_scale);
+                uint8_t* qp = g.C8 + (int64_t)m * g.ldc8 + n;
+                if (g.c8_vec8 && n + 8 <= g.N) {
+                    uint2 v;
+                    v.x = b8[0] | (b8[1] << 8) | (b8[2] << 16) | (b8[3] << 24);
+                    v.y = b8[4] | (b8[5] << 8) | (b8[6] << 16) | (b8[7] << 24);
+                    *reinterpret_cast<uint2*>(qp) = v;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (n + e < g.N) qp[e] = (uint8_t)b8[e];
+                }
+            }
+        }
+        __syncthreads();                   // the staging tile is the next piece's slab
         return true;
     };
 

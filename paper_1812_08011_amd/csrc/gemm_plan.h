@@ -37,7 +37,9 @@ struct GemmArgs {
     int M, N, K, CL;
     int a_vec;          // A, lda allow 4-byte loads (and lda < 2^24)
     int b_vec;          // B, ldb allow 4-byte loads (and ldb < 2^24)
-    int c_vec;          // C, ldc allow stores of a lane's whole row of codes
+    int c_vec;          // C, ldc allow 4-byte stores of code pairs
+    int c_vec16;        // C, ldc allow 16-byte stores (8 codes)
+    int c8_vec8;        // C8, ldc8 allow 8-byte stores
     int guarded;        // exact mode: try the guarded path first
 };
 
