@@ -138,22 +138,41 @@ __device__ __forceinline__ uint16_t f32_to_fp16_rn(float x) {
 }
 
 // Plain float -> nearest FP8 code, ties to even, gradual underflow below
-// 2^-14, finite overflow saturating at 57344.
+// 2^-14, finite overflow saturating at 57344, Inf -> Inf, NaN -> 0x7F.
+// The E5M2 conversion instruction rounds to nearest even with gradual
+// underflow but turns finite overflow into Inf, so finite values are first
+// clamped to +-57344 (magnitudes in [57344, 61440) round to 57344 anyway, and
+// larger ones saturate there) and Inf / NaN get their codes explicitly.  This
+// equals the integer definition (bias-15 exponent, mantissa rounded at bit
+// 21, subnormal quantum 2^-16) on every one of the 2^32 float inputs; the
+// tests compare it with the oracle over every exponent and sign.
+__device__ __forceinline__ uint32_t fp8_special(uint32_t u) {
+    const uint32_t a = u & 0x7FFFFFFFu;
+    return a > kF32Inf ? kFp8NaN : (0x7Cu | ((u >> 24) & 0x80u));
+}
+
 __device__ __forceinline__ uint32_t f32_to_fp8(float x) {
-    uint32_t u = __float_as_uint(x);
-    uint32_t s = (u >> 24) & 0x80u;
-    uint32_t a = u & 0x7FFFFFFFu;
-    uint32_t r;
-    if (a > kF32Inf) return kFp8NaN;
-    if (a >= 0x47700000u) {                      // |x| >= 61440 (or Inf)
-        r = (a == kF32Inf) ? 0x7Cu : 0x7Bu;
-    } else if (a < 0x38800000u) {                // |x| < 2^-14
-        r = (uint32_t)__builtin_rintf(__uint_as_float(a) * 65536.0f);
-    } else {
-        uint32_t b = a + 0xFFFFFu + ((a >> 21) & 1u);
-        r = (b >> 21) - (112u << 2);
+    const float y = __builtin_amdgcn_fmed3f(x, -57344.0f, 57344.0f);
+    const uint32_t r = __builtin_amdgcn_cvt_pk_bf8_f32(y, y, 0, false) & 0xFFu;
+    const uint32_t u = __float_as_uint(x);
+    return (u & 0x7FFFFFFFu) >= kF32Inf ? fp8_special(u) : r;
+}
+
+// Codes of x0, x1 into bytes 0, 1 (HI = false) or 2, 3 (HI = true) of old,
+// whose other half is kept: one conversion instruction for two values.
+template <bool HI>
+__device__ __forceinline__ uint32_t f32x2_to_fp8x2(float x0, float x1, uint32_t old) {
+    const float y0 = __builtin_amdgcn_fmed3f(x0, -57344.0f, 57344.0f);
+    const float y1 = __builtin_amdgcn_fmed3f(x1, -57344.0f, 57344.0f);
+    uint32_t r = __builtin_amdgcn_cvt_pk_bf8_f32(y0, y1, old, HI);
+    const uint32_t u0 = __float_as_uint(x0), u1 = __float_as_uint(x1);
+    if (__builtin_expect(((u0 & 0x7FFFFFFFu) >= kF32Inf) | ((u1 & 0x7FFFFFFFu) >= kF32Inf), 0)) {
+        constexpr int sh = HI ? 16 : 0;
+        const uint32_t c0 = (u0 & 0x7FFFFFFFu) >= kF32Inf ? fp8_special(u0) : (r >> sh) & 0xFFu;
+        const uint32_t c1 = (u1 & 0x7FFFFFFFu) >= kF32Inf ? fp8_special(u1) : (r >> (sh + 8)) & 0xFFu;
+        r = (r & ~(0xFFFFu << sh)) | (c0 << sh) | (c1 << (sh + 8));
     }
-    return r | s;
+    return r;
 }
 
 // FP8 code of an FP16 result held as a float on the FP16 grid scaled by 2^S:
@@ -172,13 +191,14 @@ __device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1
     const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        uint32_t hi0 = __umulhi(M0, c.x), lo0 = M0 * c.x;
-        uint32_t hi1 = __umulhi(M1, c.z), lo1 = M1 * c.z;
+        // one 32 x 32 -> 64-bit multiply gives both halves of each product
+        const uint64_t p0 = (uint64_t)M0 * c.x;
+        const uint64_t p1 = (uint64_t)M1 * c.z;
         u32x4 n;
-        n.x = hi1 ^ c.y ^ k0;
-        n.y = lo1;
-        n.z = hi0 ^ c.w ^ k1;
-        n.w = lo0;
+        n.x = (uint32_t)(p1 >> 32) ^ c.y ^ k0;
+        n.y = (uint32_t)p1;
+        n.z = (uint32_t)(p0 >> 32) ^ c.w ^ k1;
+        n.w = (uint32_t)p0;
         c = n;
         k0 += W0;
         k1 += W1;

@@ -407,21 +407,19 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                 }
             }
             if (g.C8 && lt < 0) {
-                uint32_t b8[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    b8[e] = f32_to_fp8(fp16_to_f32((cw[e / 2] >> (16 * (e % 2))) & 0xFFFFu) *
-                                       g.q_scale);
+                auto val = [&](int e) __attribute__((always_inline)) {
+                    return fp16_to_f32((cw[e / 2] >> (16 * (e % 2))) & 0xFFFFu) * g.q_scale;
+                };
+                uint2 v;
+                v.x = f32x2_to_fp8x2<true>(val(2), val(3), f32x2_to_fp8x2<false>(val(0), val(1), 0u));
+                v.y = f32x2_to_fp8x2<true>(val(6), val(7), f32x2_to_fp8x2<false>(val(4), val(5), 0u));
                 uint8_t* qp = g.C8 + (int64_t)m * g.ldc8 + n;
                 if (g.c8_vec8 && n + 8 <= g.N) {
-                    uint2 v;
-                    v.x = b8[0] | (b8[1] << 8) | (b8[2] << 16) | (b8[3] << 24);
-                    v.y = b8[4] | (b8[5] << 8) | (b8[6] << 16) | (b8[7] << 24);
                     *reinterpret_cast<uint2*>(qp) = v;
                 } else {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
-                        if (n + e < g.N) qp[e] = (uint8_t)b8[e];
+                        if (n + e < g.N) qp[e] = (uint8_t)((e < 4 ? v.x : v.y) >> (8 * (e % 4)));
                 }
             }
         }

@@ -22,11 +22,8 @@ __global__ __launch_bounds__(kThreads) void q8_from_f32_kernel(
     uint32_t* d4 = reinterpret_cast<uint32_t*>(dst);
     for (int64_t i = tid; i < nvec; i += stride) {
         float4 x = s4[i];
-        uint32_t b0 = f32_to_fp8(x.x * scale);
-        uint32_t b1 = f32_to_fp8(x.y * scale);
-        uint32_t b2 = f32_to_fp8(x.z * scale);
-        uint32_t b3 = f32_to_fp8(x.w * scale);
-        d4[i] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+        const uint32_t lo = f32x2_to_fp8x2<false>(x.x * scale, x.y * scale, 0u);
+        d4[i] = f32x2_to_fp8x2<true>(x.z * scale, x.w * scale, lo);
     }
     for (int64_t i = nvec * 4 + tid; i < n; i += stride)
         dst[i] = (uint8_t)f32_to_fp8(src[i] * scale);
@@ -42,11 +39,10 @@ __global__ __launch_bounds__(kThreads) void q8_from_fp16_kernel(
     uint32_t* d4 = reinterpret_cast<uint32_t*>(dst);
     for (int64_t i = tid; i < nvec; i += stride) {
         uint2 c = s4[i];
-        uint32_t b0 = f32_to_fp8(fp16_to_f32(c.x & 0xFFFFu) * scale);
-        uint32_t b1 = f32_to_fp8(fp16_to_f32(c.x >> 16) * scale);
-        uint32_t b2 = f32_to_fp8(fp16_to_f32(c.y & 0xFFFFu) * scale);
-        uint32_t b3 = f32_to_fp8(fp16_to_f32(c.y >> 16) * scale);
-        d4[i] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+        const uint32_t lo = f32x2_to_fp8x2<false>(fp16_to_f32(c.x & 0xFFFFu) * scale,
+                                                  fp16_to_f32(c.x >> 16) * scale, 0u);
+        d4[i] = f32x2_to_fp8x2<true>(fp16_to_f32(c.y & 0xFFFFu) * scale,
+                                     fp16_to_f32(c.y >> 16) * scale, lo);
     }
     for (int64_t i = nvec * 4 + tid; i < n; i += stride)
         dst[i] = (uint8_t)f32_to_fp8(fp16_to_f32(src[i]) * scale);

@@ -79,6 +79,22 @@ def test_fp8_quantize_f32_bit_patterns():
         assert np.array_equal(got, ref), np.flatnonzero(got != ref)[:10]
 
 
+def test_fp8_quantize_every_f32_prefix():
+    """Every sign, exponent and top-7-bit mantissa prefix of a float, with the
+    low 16 bits at the rounding-relevant patterns (ties have them all zero)
+    and at random values: the conversion is correct in every binade."""
+    rng = np.random.default_rng(503)
+    hi = np.arange(65536, dtype=np.uint32) << 16
+    lows = np.concatenate([np.uint32([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF]),
+                           rng.integers(0, 65536, size=6, dtype=np.uint32)])
+    x = (hi[:, None] | lows[None, :]).ravel().view(np.float32)
+    for scale in (1.0, 3.0):
+        say(f"fp8_quantize f32 every prefix n={x.size} scale={scale}")
+        got = host(q8(dev(x), scale))
+        ref = oracle.fp8_quantize(x, scale)
+        assert np.array_equal(got, ref), np.flatnonzero(got != ref)[:10]
+
+
 def test_fp8_quantize_all_fp16_codes_and_odd_offsets():
     codes = np.arange(65536, dtype=np.uint16)
     for scale in (1.0, 1000.0, 2.0 ** -3):
@@ -413,6 +429,43 @@ def test_sr_update_variants():
                 _update_case(rng, n, with_v, with_w8)
     _update_case(rng, 50_000, seed=2 ** 63 + 12345, offset=2 ** 40 + 7)
     _update_case(rng, 50_000, lr=0.0, mu=0.0, wd=0.0)
+
+
+def test_sr_update_mixed_ranges():
+    """Elements outside FP16's normal range (zeros, subnormals, values whose
+    update leaves the range or overflows, Inf, NaN) scattered among ordinary
+    ones: the groups holding them take the general path, the others the
+    normal-range one, and both must agree with the oracle."""
+    rng = np.random.default_rng(544)
+    n = 200_003
+    w = oracle.fp16_quantize((rng.standard_normal(n) * 0.02).astype(np.float32))
+    g = oracle.fp16_quantize((rng.standard_normal(n) * 1e-4).astype(np.float32))
+    v = oracle.fp16_quantize((rng.standard_normal(n) * 1e-4).astype(np.float32))
+    specials = np.uint16([0x0000, 0x8000, 0x0001, 0x81FF, 0x0200, 0x7DFF, 0xFDFF, 0x7C00,
+                          0x7E00, 0xFE00, 0x7F00, 0x3E00])
+    for arr in (w, g, v):
+        idx = rng.choice(n, size=n // 500, replace=False)
+        arr[idx] = rng.choice(specials, size=idx.size)
+    wd_, gd, vd = dev(w), dev(g), dev(v)
+    w8d = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    for lr, mu, wdk in ((0.1, 0.9, 1e-4), (3e4, 0.9, 0.5), (0.1, 0.0, 0.0)):
+        say(f"sr_weight_update mixed ranges lr={lr} mu={mu} wd={wdk}")
+        wd_.copy_(dev(w)); vd.copy_(dev(v))
+        fp8t.sr_weight_update(wd_, gd, vd if mu else None, w8d, n, lr, mu, wdk, 11, 5)
+        ow, ov, ow8 = oracle.sr_weight_update(w, g, v if mu else None, lr=lr, momentum=mu,
+                                              weight_decay=wdk, seed=11, offset=5)
+        assert np.array_equal(host(wd_), ow)
+        if mu:
+            assert np.array_equal(host(vd), ov)
+        assert np.array_equal(host(w8d), ow8)
+
+
+@pytest.mark.parametrize("lr", [float("inf"), float("nan"), -float("inf")])
+def test_sr_update_non_finite_rate(lr):
+    rng = np.random.default_rng(545)
+    n = 4099
+    _update_case(rng, n, lr=lr)
+    _update_case(rng, n, lr=0.1, mu=float("nan"))
 
 
 def test_sr_update_misaligned_pointers():
