@@ -136,56 +136,81 @@ __device__ __forceinline__ bool update_pair_normal(const u32x4& rnd, uint32_t wp
     return lo >= 0x1p-30f && hi < 0x1p31f;
 }
 
-// One thread updates kPairs consecutive element pairs.  When the tensors
-// allow it, that is one 16-byte load of each of w, g, v and 16-byte stores of
-// w, v plus an 8-byte store of w8; pairs at the ragged end, or all pairs when
-// a pointer is not aligned for those widths, are handled element by element.
-constexpr int kPairs = 4;
+// One thread updates PAIRS consecutive element pairs (PAIRS = 1, 2 or 4).
+// When the tensors allow it, that is one 4 * PAIRS-byte load of each of w, g,
+// v, stores of the same width of w, v and a 2 * PAIRS-byte store of w8; pairs
+// at the ragged end, or all pairs when a pointer is not aligned for those
+// widths, are handled element by element.  Four pairs per thread suit large
+// tensors (wider memory operations); one pair per thread keeps small ones
+// spread over the whole chip.
+template <int PAIRS> struct Words;
+template <> struct Words<1> { typedef uint32_t t16; typedef uint16_t t8; };
+template <> struct Words<2> { typedef uint2 t16; typedef uint32_t t8; };
+template <> struct Words<4> { typedef uint4 t16; typedef uint2 t8; };
 
-template <bool HAS_V, bool HAS_W8>
+template <int PAIRS>
+__device__ __forceinline__ void vload(const uint16_t* p, int64_t q, uint32_t (&o)[PAIRS]) {
+    const typename Words<PAIRS>::t16 x = reinterpret_cast<const typename Words<PAIRS>::t16*>(p)[q];
+    __builtin_memcpy(o, &x, sizeof(x));
+}
+template <int PAIRS>
+__device__ __forceinline__ void vstore(uint16_t* p, int64_t q, const uint32_t (&o)[PAIRS]) {
+    typename Words<PAIRS>::t16 x;
+    __builtin_memcpy(&x, o, sizeof(x));
+    reinterpret_cast<typename Words<PAIRS>::t16*>(p)[q] = x;
+}
+
+template <bool HAS_V, bool HAS_W8, int PAIRS>
 __global__ __launch_bounds__(kThreads) void sr_update_kernel(
     uint16_t* __restrict__ w, const uint16_t* __restrict__ g, uint16_t* __restrict__ v,
     uint8_t* __restrict__ w8, int64_t n, upd_params p, int vec_ok) {
+    constexpr int NQ = (PAIRS + 1) / 2;          // 32-bit words of FP8 codes
     const int64_t npairs = (n + 1) / 2;
-    const int64_t ngroups = (npairs + kPairs - 1) / kPairs;
+    const int64_t ngroups = (npairs + PAIRS - 1) / PAIRS;
     const int64_t stride = (int64_t)gridDim.x * kThreads;
     for (int64_t q = (int64_t)blockIdx.x * kThreads + threadIdx.x; q < ngroups; q += stride) {
-        const int64_t pr0 = q * kPairs;
-        if (vec_ok && 2 * (pr0 + kPairs) <= n) {
-            const uint4 wv = reinterpret_cast<const uint4*>(w)[q];
-            const uint4 gv = reinterpret_cast<const uint4*>(g)[q];
-            uint4 vv = {0u, 0u, 0u, 0u};
-            if (HAS_V) vv = reinterpret_cast<const uint4*>(v)[q];
-            const uint32_t wa[4] = {wv.x, wv.y, wv.z, wv.w};
-            const uint32_t ga[4] = {gv.x, gv.y, gv.z, gv.w};
-            const uint32_t va[4] = {vv.x, vv.y, vv.z, vv.w};
-            uint32_t wo[4], vo[4], qo[2];
-            float w1[4][2];
+        const int64_t pr0 = q * PAIRS;
+        if (vec_ok && 2 * (pr0 + PAIRS) <= n) {
+            uint32_t wa[PAIRS], ga[PAIRS], va[PAIRS];
+            vload<PAIRS>(w, q, wa);
+            vload<PAIRS>(g, q, ga);
+#pragma unroll
+            for (int j = 0; j < PAIRS; ++j) va[j] = 0u;
+            if (HAS_V) vload<PAIRS>(v, q, va);
+            uint32_t wo[PAIRS], vo[PAIRS], qo[NQ];
+            float w1[PAIRS][2];
             bool ok = p.finite;
 #pragma unroll
-            for (int j = 0; j < kPairs; ++j)
+            for (int j = 0; j < PAIRS; ++j)
                 ok &= update_pair_normal<HAS_V>(pair_bits((uint64_t)(pr0 + j), p), wa[j], ga[j],
                                                 va[j], p, wo[j], vo[j], w1[j]);
             if (__builtin_expect(ok, 1)) {
-                qo[0] = f32x2_to_fp8x2<true>(w1[1][0], w1[1][1],
-                                             f32x2_to_fp8x2<false>(w1[0][0], w1[0][1], 0u));
-                qo[1] = f32x2_to_fp8x2<true>(w1[3][0], w1[3][1],
-                                             f32x2_to_fp8x2<false>(w1[2][0], w1[2][1], 0u));
+#pragma unroll
+                for (int k = 0; k < NQ; ++k) {
+                    qo[k] = f32x2_to_fp8x2<false>(w1[2 * k][0], w1[2 * k][1], 0u);
+                    if (2 * k + 1 < PAIRS)
+                        qo[k] = f32x2_to_fp8x2<true>(w1[2 * k + 1][0], w1[2 * k + 1][1], qo[k]);
+                }
             } else {
-                uint32_t q8[4];
-                for (int j = 0; j < kPairs; ++j)
+#pragma unroll
+                for (int k = 0; k < NQ; ++k) qo[k] = 0u;
+                for (int j = 0; j < PAIRS; ++j) {
+                    uint32_t q8;
                     update_pair<HAS_V>(pair_bits((uint64_t)(pr0 + j), p), wa[j], ga[j], va[j], p,
-                                       wo[j], vo[j], q8[j]);
-                qo[0] = q8[0] | (q8[1] << 16);
-                qo[1] = q8[2] | (q8[3] << 16);
+                                       wo[j], vo[j], q8);
+                    qo[j / 2] |= q8 << (16 * (j % 2));
+                }
             }
-            reinterpret_cast<uint4*>(w)[q] = make_uint4(wo[0], wo[1], wo[2], wo[3]);
-            if (HAS_V) reinterpret_cast<uint4*>(v)[q] = make_uint4(vo[0], vo[1], vo[2], vo[3]);
-            if (HAS_W8)
-                reinterpret_cast<uint2*>(w8)[q] = make_uint2(qo[0], qo[1]);
+            vstore<PAIRS>(w, q, wo);
+            if (HAS_V) vstore<PAIRS>(v, q, vo);
+            if (HAS_W8) {
+                typename Words<PAIRS>::t8 x;
+                __builtin_memcpy(&x, qo, sizeof(x));
+                reinterpret_cast<typename Words<PAIRS>::t8*>(w8)[q] = x;
+            }
             continue;
         }
-        for (int j = 0; j < kPairs; ++j) {
+        for (int j = 0; j < PAIRS; ++j) {
             const int64_t pr = pr0 + j;
             if (pr >= npairs) break;
             const int64_t i = 2 * pr;
@@ -229,20 +254,27 @@ extern "C" int sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v, uin
     p.off_lo = (uint32_t)offset;
     p.off_hi = (uint32_t)(offset >> 32);
     p.finite = std::isfinite(lr) && std::isfinite(momentum) && std::isfinite(weight_decay);
-    const int vec_ok = aligned(w, 16) && aligned(g, 16) && (!v || aligned(v, 16)) &&
-                       (!w8 || aligned(w8, 8));
     const int64_t npairs = (n + 1) / 2;
-    const int64_t nthreads = (npairs + kPairs - 1) / kPairs;
+    // four pairs per thread once that still gives every CU 2048 threads
+    const int pairs = npairs >= 4 * (int64_t)256 * 2048 ? 4 : 1;
+    const int wb = 4 * pairs;                   // bytes of w, g, v per thread
+    const int vec_ok = aligned(w, wb) && aligned(g, wb) && (!v || aligned(v, wb)) &&
+                       (!w8 || aligned(w8, wb / 2));
+    const int64_t nthreads = (npairs + pairs - 1) / pairs;
     int64_t groups = (nthreads + kThreads - 1) / kThreads;
     if (groups > 256 * 32) groups = 256 * 32;
     const dim3 grid((unsigned)groups), block(kThreads);
-#define FP8T_LAUNCH(HV, HW)                                                       \
-    hipLaunchKernelGGL((sr_update_kernel<HV, HW>), grid, block, 0, stream, w, g, v, \
-                       w8, n, p, vec_ok)
-    if (v && w8) FP8T_LAUNCH(true, true);
-    else if (v) FP8T_LAUNCH(true, false);
-    else if (w8) FP8T_LAUNCH(false, true);
-    else FP8T_LAUNCH(false, false);
+#define FP8T_LAUNCH(HV, HW)                                                                \
+    if (pairs == 4)                                                                        \
+        hipLaunchKernelGGL((sr_update_kernel<HV, HW, 4>), grid, block, 0, stream, w, g, v, \
+                           w8, n, p, vec_ok);                                              \
+    else                                                                                   \
+        hipLaunchKernelGGL((sr_update_kernel<HV, HW, 1>), grid, block, 0, stream, w, g, v, \
+                           w8, n, p, vec_ok)
+    if (v && w8) { FP8T_LAUNCH(true, true); }
+    else if (v) { FP8T_LAUNCH(true, false); }
+    else if (w8) { FP8T_LAUNCH(false, true); }
+    else { FP8T_LAUNCH(false, false); }
 #undef FP8T_LAUNCH
     return launch_status();
 }

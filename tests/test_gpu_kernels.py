@@ -431,13 +431,14 @@ def test_sr_update_variants():
     _update_case(rng, 50_000, lr=0.0, mu=0.0, wd=0.0)
 
 
-def test_sr_update_mixed_ranges():
+@pytest.mark.parametrize("n", [200_003, 4_500_001])
+def test_sr_update_mixed_ranges(n):
     """Elements outside FP16's normal range (zeros, subnormals, values whose
     update leaves the range or overflows, Inf, NaN) scattered among ordinary
     ones: the groups holding them take the general path, the others the
-    normal-range one, and both must agree with the oracle."""
+    normal-range one, and both must agree with the oracle (one pair per
+    thread at the smaller size, four at the larger)."""
     rng = np.random.default_rng(544)
-    n = 200_003
     w = oracle.fp16_quantize((rng.standard_normal(n) * 0.02).astype(np.float32))
     g = oracle.fp16_quantize((rng.standard_normal(n) * 1e-4).astype(np.float32))
     v = oracle.fp16_quantize((rng.standard_normal(n) * 1e-4).astype(np.float32))
@@ -449,7 +450,7 @@ def test_sr_update_mixed_ranges():
     wd_, gd, vd = dev(w), dev(g), dev(v)
     w8d = torch.zeros(n, dtype=torch.uint8, device=DEV)
     for lr, mu, wdk in ((0.1, 0.9, 1e-4), (3e4, 0.9, 0.5), (0.1, 0.0, 0.0)):
-        say(f"sr_weight_update mixed ranges lr={lr} mu={mu} wd={wdk}")
+        say(f"sr_weight_update mixed ranges n={n} lr={lr} mu={mu} wd={wdk}")
         wd_.copy_(dev(w)); vd.copy_(dev(v))
         fp8t.sr_weight_update(wd_, gd, vd if mu else None, w8d, n, lr, mu, wdk, 11, 5)
         ow, ov, ow8 = oracle.sr_weight_update(w, g, v if mu else None, lr=lr, momentum=mu,
