@@ -68,6 +68,14 @@ def lib():
         L.cpu_chunk_gemm_points.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64,
                                             i64, vp, i64, vp, i64, ctypes.c_int,
                                             vp, vp, i64, vp]
+        u32 = ctypes.c_uint32
+        L.cpu_chunk_gemm_sr.restype = ctypes.c_int
+        L.cpu_chunk_gemm_sr.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64, i64,
+                                        vp, i64, vp, i64, vp, i64, u64, u32]
+        L.cpu_chunk_gemm_sr_points.restype = ctypes.c_int
+        L.cpu_chunk_gemm_sr_points.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64,
+                                               i64, vp, i64, vp, i64, u64, u32,
+                                               vp, vp, i64, vp]
         L.cpu_sr_weight_update.restype = ctypes.c_int
         L.cpu_sr_weight_update.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, u64, u64]
         L.orc_num_threads.restype = ctypes.c_int
@@ -200,6 +208,37 @@ def chunk_gemm_points(A, B, CL, rows, cols, trans_a=0, trans_b=0, mode=EXACT):
                                        _ptr(A), lda, _ptr(B), ldb, int(mode),
                                        _ptr(rows), _ptr(cols), rows.size, _ptr(out)),
            "chunk_gemm_points")
+    return out
+
+
+def chunk_gemm_sr(A, B, CL, trans_a=0, trans_b=0, *, seed, offset=0):
+    """chunk_gemm with stochastic rounding after every P16 addition."""
+    A = np.ascontiguousarray(A, dtype=np.uint8)
+    B = np.ascontiguousarray(B, dtype=np.uint8)
+    M, N, K = _gemm_dims(trans_a, trans_b, A, B)
+    C = np.zeros((M, N), dtype=np.uint16)
+    lda = A.shape[1] if A.shape[1] > 0 else 1
+    ldb = B.shape[1] if B.shape[1] > 0 else 1
+    _check(lib().cpu_chunk_gemm_sr(int(trans_a), int(trans_b), M, N, K, int(CL), _ptr(A), lda,
+                                   _ptr(B), ldb, _ptr(C), max(N, 1), int(seed), int(offset)),
+           "chunk_gemm_sr")
+    return C
+
+
+def chunk_gemm_sr_points(A, B, CL, rows, cols, trans_a=0, trans_b=0, *, seed, offset=0):
+    """chunk_gemm_sr at the outputs (rows[p], cols[p]) only."""
+    A = np.ascontiguousarray(A, dtype=np.uint8)
+    B = np.ascontiguousarray(B, dtype=np.uint8)
+    M, N, K = _gemm_dims(trans_a, trans_b, A, B)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    out = np.zeros(rows.size, dtype=np.uint16)
+    lda = A.shape[1] if A.shape[1] > 0 else 1
+    ldb = B.shape[1] if B.shape[1] > 0 else 1
+    _check(lib().cpu_chunk_gemm_sr_points(int(trans_a), int(trans_b), M, N, K, int(CL),
+                                          _ptr(A), lda, _ptr(B), ldb, int(seed), int(offset),
+                                          _ptr(rows), _ptr(cols), rows.size, _ptr(out)),
+           "chunk_gemm_sr_points")
     return out
 
 

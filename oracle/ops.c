@@ -147,6 +147,97 @@ int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
     return ORC_OK;
 }
 
+/* ---- chunk-based accumulation with stochastic rounding -------------------
+ * Sec. 2.3 names two rounding modes after P16 additions -- nearest and
+ * stochastic -- and Fig. 3(b) compares them on long accumulations.  This is
+ * the chunk-based dot product of Fig. 3(a) with every P16 addition rounded
+ * stochastically instead of to nearest: the sum of the running value and the
+ * next term is first formed in FP32 (the intermediate sum held with k' = 23
+ * mantissa bits) and then rounded into P16 by Eq. (1) (orc_sr16):
+ *     P = SR16(fl32(P + a(i,k) b(k,j)))   for k in the chunk, ascending
+ *     S = SR16(fl32(S + P))                after each chunk
+ * (products of two P8 values are exact in FP32, so fl32 is one rounding of
+ * the exact sum).  CL >= K is plain sequential accumulation with stochastic
+ * rounding, the SR curve of Fig. 3(b).
+ * Random bits (the paper names no source): Philox4x32-10 with key = seed and
+ * 16-bit uniforms taken from each 32-bit word, low half first.  The addition
+ * of product k into output (i, j) uses uniform k mod 8 of the block with
+ * counter (i, j, k / 8, 2 * offset); the addition of chunk c into the running
+ * sum uses the low half of word 0 of the block with counter
+ * (i, j, c, 2 * offset + 1). */
+static uint32_t sr_uniform(uint32_t i, uint32_t j, uint32_t q, uint32_t w3,
+                           int idx, const uint32_t key[2]) {
+    const uint32_t ctr[4] = {i, j, q, w3};
+    uint32_t words[4];
+    orc_philox4x32_10(ctr, key, words);
+    const uint32_t word = words[idx / 2];
+    return (idx % 2) ? (word >> 16) : (word & 0xFFFFu);
+}
+
+static uint16_t chunk_dot_sr(int trans_a, int trans_b, int64_t K, int64_t CL,
+                             const uint8_t* A, int64_t lda, const uint8_t* B,
+                             int64_t ldb, uint64_t seed, uint32_t offset,
+                             int64_t i, int64_t j) {
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint16_t S = 0;                                   /* +0 */
+    int64_t c = 0;
+    for (int64_t c0 = 0; c0 < K; c0 += CL, c++) {
+        int64_t c1 = (K - c0 < CL) ? K : c0 + CL;
+        uint16_t P = 0;
+        for (int64_t k = c0; k < c1; k++) {
+            float p = (float)orc_p16_value(orc_mul8(op_a(trans_a, A, lda, i, k),
+                                                    op_b(trans_b, B, ldb, k, j)));
+            volatile float x = (float)orc_p16_value(P) + p;      /* fl32 */
+            P = orc_sr16(x, sr_uniform((uint32_t)i, (uint32_t)j, (uint32_t)(k / 8),
+                                       2u * offset, (int)(k % 8), key));
+        }
+        volatile float x = (float)orc_p16_value(S) + (float)orc_p16_value(P);
+        S = orc_sr16(x, sr_uniform((uint32_t)i, (uint32_t)j, (uint32_t)c,
+                                   2u * offset + 1u, 0, key));
+    }
+    return S;
+}
+
+static int sr_args_ok(int64_t M, int64_t N, int64_t K, uint32_t offset) {
+    return M <= ((int64_t)1 << 32) && N <= ((int64_t)1 << 32) &&
+           K / 8 < ((int64_t)1 << 32) && offset < 0x80000000u;
+}
+
+int cpu_chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                      int64_t CL, const uint8_t* A, int64_t lda,
+                      const uint8_t* B, int64_t ldb, uint16_t* C, int64_t ldc,
+                      uint64_t seed, uint32_t offset) {
+    if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, ORC_EXACT))
+        return ORC_EINVAL;
+    if (!sr_args_ok(M, N, K, offset)) return ORC_EINVAL;
+    if (M > 0 && N > 0 && (!C || ldc < N)) return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; i++)
+        for (int64_t j = 0; j < N; j++)
+            C[i * ldc + j] = chunk_dot_sr(trans_a, trans_b, K, CL, A, lda, B, ldb,
+                                          seed, offset, i, j);
+    return ORC_OK;
+}
+
+int cpu_chunk_gemm_sr_points(int trans_a, int trans_b, int64_t M, int64_t N,
+                             int64_t K, int64_t CL, const uint8_t* A, int64_t lda,
+                             const uint8_t* B, int64_t ldb, uint64_t seed,
+                             uint32_t offset, const int64_t* rows,
+                             const int64_t* cols, int64_t npts, uint16_t* out) {
+    if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, ORC_EXACT))
+        return ORC_EINVAL;
+    if (!sr_args_ok(M, N, K, offset)) return ORC_EINVAL;
+    if (npts < 0 || (npts > 0 && (!rows || !cols || !out))) return ORC_EINVAL;
+    for (int64_t p = 0; p < npts; p++)
+        if (rows[p] < 0 || rows[p] >= M || cols[p] < 0 || cols[p] >= N)
+            return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t p = 0; p < npts; p++)
+        out[p] = chunk_dot_sr(trans_a, trans_b, K, CL, A, lda, B, ldb, seed, offset,
+                              rows[p], cols[p]);
+    return ORC_OK;
+}
+
 /* ---- SGD weight update in P16 with stochastic rounding -------------------
  * Sec. 2.2 (Fig. 2(b)) and Sec. 4.3: the three AXPYs of an SGD step --
  * L2 regularisation, momentum accumulation and the weight update -- all run

@@ -66,6 +66,19 @@ int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
                           const int64_t* rows, const int64_t* cols,
                           int64_t npts, uint16_t* out);
 
+/* chunk_gemm with stochastic instead of nearest rounding after every P16
+ * addition (Sec. 2.3, Fig. 3(b)); random bits keyed by (seed, i, j, k) as
+ * described in ops.c.  Requires M, N <= 2^32, K / 8 < 2^32, offset < 2^31. */
+int cpu_chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                      int64_t CL, const uint8_t* A, int64_t lda,
+                      const uint8_t* B, int64_t ldb, uint16_t* C, int64_t ldc,
+                      uint64_t seed, uint32_t offset);
+int cpu_chunk_gemm_sr_points(int trans_a, int trans_b, int64_t M, int64_t N,
+                             int64_t K, int64_t CL, const uint8_t* A, int64_t lda,
+                             const uint8_t* B, int64_t ldb, uint64_t seed,
+                             uint32_t offset, const int64_t* rows,
+                             const int64_t* cols, int64_t npts, uint16_t* out);
+
 int cpu_sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v,
                          uint8_t* w8, int64_t n, float lr, float momentum,
                          float weight_decay, uint64_t seed, uint64_t offset);
