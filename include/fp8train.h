@@ -162,6 +162,45 @@ size_t chunk_gemm_fp8_workspace_size(int trans_a, int trans_b, int64_t M,
                                      int64_t N, int64_t K, int64_t CL, int mode);
 
 /*
+ * chunk_gemm_sr -- chunk_gemm (FP8T_EXACT layouts and chunking) with every
+ * FP16 addition rounded stochastically instead of to nearest: the second
+ * rounding mode after FP16 additions of Sec. 2.3, whose effect on long
+ * accumulations Fig. 3(b) shows.
+ *
+ * For every output (i, j), with a(k), b(k) as in chunk_gemm:
+ *   within chunk c (ascending k):  P = SR(fl32(P + a(k) * b(k)))
+ *   after chunk c:                 S = SR(fl32(S + P))
+ *   P and S start at +0; C(i, j) = the FP16 code of S (+0 when K == 0).
+ * fl32 is one IEEE single-precision addition (the product is exact), and SR
+ * is sr_weight_update's stochastic rounding into FP16 (Eq. (1), k = 9 of
+ * k' = 23 bits, 16-bit uniform u: the magnitude is rounded up iff
+ * u < 2^16 x the discarded fraction of a step).  The uniforms come from
+ * Philox4x32-10 with key = (seed low, seed high), 16-bit halves of each word,
+ * low half first: the addition of product k into output (i, j) uses uniform
+ * k mod 8 of the block with counter (i, j, k / 8, 2 * offset), the addition
+ * of chunk c into the running sum the low half of word 0 of the block with
+ * counter (i, j, c, 2 * offset + 1).  The result is a pure function of the
+ * inputs, seed and offset (bit-exact, independent of the device and plan).
+ *
+ * Layouts, CL, C and the workspace contract are those of chunk_gemm (with
+ * chunk_gemm_sr_workspace_size as the query).  offset < 2^31.
+ * Errors: as chunk_gemm, and FP8T_EINVAL for offset >= 2^31.
+ */
+int chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                  int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+                  int64_t ldb, uint16_t* C, int64_t ldc, uint64_t seed,
+                  uint64_t offset, void* workspace, size_t workspace_bytes,
+                  hipStream_t stream);
+
+/*
+ * chunk_gemm_sr_workspace_size -- bytes of workspace the fastest plan of
+ * chunk_gemm_sr needs on the current device for these arguments (0 if none,
+ * or for invalid arguments).
+ */
+size_t chunk_gemm_sr_workspace_size(int trans_a, int trans_b, int64_t M,
+                                    int64_t N, int64_t K, int64_t CL);
+
+/*
  * sr_weight_update -- one SGD step entirely in FP16 with floating-point
  * stochastic rounding (Sec. 2.2 / Fig. 2(b): L2-Reg, Momentum-Acc and
  * Weight-Upd AXPYs; Sec. 2.3 Eq. (1); Sec. 4.3), keeping the FP16 master

@@ -160,11 +160,13 @@ int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
  * the exact sum).  CL >= K is plain sequential accumulation with stochastic
  * rounding, the SR curve of Fig. 3(b).
  * Random bits (the paper names no source): Philox4x32-10 with key = seed and
- * 16-bit uniforms taken from each 32-bit word, low half first.  The addition
- * of product k into output (i, j) uses uniform k mod 8 of the block with
- * counter (i, j, k / 8, 2 * offset); the addition of chunk c into the running
- * sum uses the low half of word 0 of the block with counter
- * (i, j, c, 2 * offset + 1). */
+ * eight 16-bit uniforms per block (the halves of its four words, low half
+ * first).  One block serves four adjacent outputs of a row for two
+ * consecutive products: the addition of product k into output (i, j) uses
+ * uniform 4 (k mod 2) + (j mod 4) of the block with counter
+ * (i, j / 4, k / 2, 2 * offset).  The addition of chunk c into the running sum
+ * of output (i, j) uses uniform j mod 8 of the block with counter
+ * (i, j / 8, c, 2 * offset + 1). */
 static uint32_t sr_uniform(uint32_t i, uint32_t j, uint32_t q, uint32_t w3,
                            int idx, const uint32_t key[2]) {
     const uint32_t ctr[4] = {i, j, q, w3};
@@ -188,19 +190,19 @@ static uint16_t chunk_dot_sr(int trans_a, int trans_b, int64_t K, int64_t CL,
             float p = (float)orc_p16_value(orc_mul8(op_a(trans_a, A, lda, i, k),
                                                     op_b(trans_b, B, ldb, k, j)));
             volatile float x = (float)orc_p16_value(P) + p;      /* fl32 */
-            P = orc_sr16(x, sr_uniform((uint32_t)i, (uint32_t)j, (uint32_t)(k / 8),
-                                       2u * offset, (int)(k % 8), key));
+            P = orc_sr16(x, sr_uniform((uint32_t)i, (uint32_t)(j / 4), (uint32_t)(k / 2),
+                                       2u * offset, (int)(4 * (k % 2) + j % 4), key));
         }
         volatile float x = (float)orc_p16_value(S) + (float)orc_p16_value(P);
-        S = orc_sr16(x, sr_uniform((uint32_t)i, (uint32_t)j, (uint32_t)c,
-                                   2u * offset + 1u, 0, key));
+        S = orc_sr16(x, sr_uniform((uint32_t)i, (uint32_t)(j / 8), (uint32_t)c,
+                                   2u * offset + 1u, (int)(j % 8), key));
     }
     return S;
 }
 
 static int sr_args_ok(int64_t M, int64_t N, int64_t K, uint32_t offset) {
     return M <= ((int64_t)1 << 32) && N <= ((int64_t)1 << 32) &&
-           K / 8 < ((int64_t)1 << 32) && offset < 0x80000000u;
+           K / 2 < ((int64_t)1 << 32) && offset < 0x80000000u;
 }
 
 int cpu_chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,

@@ -68,7 +68,7 @@ int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
 
 /* chunk_gemm with stochastic instead of nearest rounding after every P16
  * addition (Sec. 2.3, Fig. 3(b)); random bits keyed by (seed, i, j, k) as
- * described in ops.c.  Requires M, N <= 2^32, K / 8 < 2^32, offset < 2^31. */
+ * described in ops.c.  Requires M, N <= 2^32, K / 2 < 2^32, offset < 2^31. */
 int cpu_chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
                       int64_t CL, const uint8_t* A, int64_t lda,
                       const uint8_t* B, int64_t ldb, uint16_t* C, int64_t ldc,

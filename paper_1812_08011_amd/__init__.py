@@ -50,6 +50,11 @@ def lib():
                                      vp, i64, f32, i32, vp, sz, vp]
         L.chunk_gemm_fp8_workspace_size.restype = sz
         L.chunk_gemm_fp8_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64, i32]
+        L.chunk_gemm_sr.restype = i32
+        L.chunk_gemm_sr.argtypes = [i32, i32, i64, i64, i64, i64, vp, i64, vp, i64, vp, i64,
+                                    u64, u64, vp, sz, vp]
+        L.chunk_gemm_sr_workspace_size.restype = sz
+        L.chunk_gemm_sr_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64]
         L.sr_weight_update.restype = i32
         L.sr_weight_update.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, u64, u64, vp]
         L.fp8t_status_string.restype = ctypes.c_char_p
@@ -145,6 +150,23 @@ def chunk_gemm_fp8(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, C8, ld
                                 int(ldc8), float(scale), int(mode), _ptr(workspace),
                                 int(workspace_bytes), _stream(stream)))
     return C8
+
+
+def chunk_gemm_sr_workspace_size(trans_a, trans_b, M, N, K, CL):
+    return int(lib().chunk_gemm_sr_workspace_size(int(trans_a), int(trans_b), int(M), int(N),
+                                                  int(K), int(CL)))
+
+
+def chunk_gemm_sr(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, seed, offset=0,
+                  workspace=None, workspace_bytes=0, stream=None):
+    """The C-ABI call with the same argument order (stochastic rounding after
+    every FP16 addition)."""
+    _check("chunk_gemm_sr",
+           lib().chunk_gemm_sr(int(trans_a), int(trans_b), int(M), int(N), int(K), int(CL),
+                               _ptr(A), int(lda), _ptr(B), int(ldb), _ptr(C), int(ldc),
+                               int(seed), int(offset), _ptr(workspace), int(workspace_bytes),
+                               _stream(stream)))
+    return C
 
 
 def sr_weight_update(w, g, v, w8, n, lr, momentum, weight_decay, seed, offset, stream=None):

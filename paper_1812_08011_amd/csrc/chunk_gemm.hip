@@ -111,45 +111,6 @@ constexpr double kClockHz = 2.4e9;      // MI355X peak engine clock
 constexpr double kLanesPerCU = 128.0;   // 32-bit VALU lane-ops per clock per CU
 constexpr double kFoldBytesPerS = 5e12; // effective HBM rate of the fold pass
 
-int env_int(const char* name, int dflt) {
-    const char* v = getenv(name);
-    return v ? atoi(v) : dflt;
-}
-
-// Compute units of the current device (cached per device).
-int device_cus() {
-    static std::mutex mu;
-    static int cached[64] = {0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    std::lock_guard<std::mutex> lk(mu);
-    if (!cached[dev]) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            return 0;
-        cached[dev] = n;
-    }
-    return cached[dev];
-}
-
-// Resident workgroups per CU of a kernel (cached per device and kernel).
-int kernel_occupancy(const void* fn, int threads) {
-    static std::mutex mu;
-    struct Ent { int dev; const void* fn; int occ; };
-    static Ent cache[256];
-    static int n = 0;
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 0;
-    std::lock_guard<std::mutex> lk(mu);
-    for (int i = 0; i < n; ++i)
-        if (cache[i].dev == dev && cache[i].fn == fn) return cache[i].occ;
-    int occ = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, fn, threads, 0) != hipSuccess)
-        return 0;
-    if (n < 256) cache[n++] = Ent{dev, fn, occ};
-    return occ;
-}
-
 // Relative cost per multiply-accumulate of each register tile on a fully
 // loaded CU, in VALU instructions (4 for the rounded FMA of the guarded path,
 // plus operand decode, LDS reads, loop overhead and lost occupancy; measured

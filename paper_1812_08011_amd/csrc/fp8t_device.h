@@ -186,6 +186,14 @@ __device__ __forceinline__ uint32_t f32d_to_fp8_scaled(float x, float scale) {
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11).
 struct u32x4 { uint32_t x, y, z, w; };
 
+// a ^ b ^ k in one instruction (gfx950's three-input bit operation; 0x96 is
+// the truth table of a three-way exclusive or), k wave-uniform.
+__device__ __forceinline__ uint32_t xor3_vvs(uint32_t a, uint32_t b, uint32_t k) {
+    uint32_t r;
+    asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(k));
+    return r;
+}
+
 __device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1) {
     const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
     const uint32_t W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
@@ -195,9 +203,9 @@ __device__ __forceinline__ u32x4 philox4x32_10(u32x4 c, uint32_t k0, uint32_t k1
         const uint64_t p0 = (uint64_t)M0 * c.x;
         const uint64_t p1 = (uint64_t)M1 * c.z;
         u32x4 n;
-        n.x = (uint32_t)(p1 >> 32) ^ c.y ^ k0;
+        n.x = xor3_vvs((uint32_t)(p1 >> 32), c.y, k0);
         n.y = (uint32_t)p1;
-        n.z = (uint32_t)(p0 >> 32) ^ c.w ^ k1;
+        n.z = xor3_vvs((uint32_t)(p0 >> 32), c.w, k1);
         n.w = (uint32_t)p0;
         c = n;
         k0 += W0;

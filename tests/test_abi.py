@@ -34,6 +34,7 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "fp8_quantize", "fp16_quantize", "chunk_gemm", "chunk_gemm_workspace_size",
         "chunk_gemm_fp8", "chunk_gemm_fp8_workspace_size",
+        "chunk_gemm_sr", "chunk_gemm_sr_workspace_size",
         "sr_weight_update", "fp8t_status_string"])
 
 
@@ -115,6 +116,32 @@ def test_chunk_gemm_fp8_rejects(lib):
     assert _gemm(lib, ws=None, wsb=64) == E
 
 
+def _gemm_sr(lib, **kw):
+    a = dict(ta=0, tb=0, M=4, N=4, K=4, CL=2, A=FAKE, lda=4, B=FAKE, ldb=4, C=FAKE, ldc=4,
+             seed=1, offset=0, ws=None, wsb=0)
+    a.update(kw)
+    return lib.chunk_gemm_sr(a["ta"], a["tb"], a["M"], a["N"], a["K"], a["CL"], a["A"], a["lda"],
+                             a["B"], a["ldb"], a["C"], a["ldc"], a["seed"], a["offset"], a["ws"],
+                             a["wsb"], None)
+
+
+def test_chunk_gemm_sr_rejects(lib):
+    E = fp8t.EINVAL
+    assert _gemm_sr(lib, CL=0) == E
+    assert _gemm_sr(lib, M=-1) == E
+    assert _gemm_sr(lib, ta=3) == E
+    assert _gemm_sr(lib, lda=3) == E
+    assert _gemm_sr(lib, ldb=3) == E
+    assert _gemm_sr(lib, ldc=3) == E
+    assert _gemm_sr(lib, C=None) == E
+    assert _gemm_sr(lib, B=None) == E
+    assert _gemm_sr(lib, offset=2 ** 31) == E
+    assert _gemm_sr(lib, K=2 ** 31) == E
+    assert _gemm_sr(lib, ws=None, wsb=64) == E
+    assert _gemm_sr(lib, M=0) == fp8t.OK
+    assert fp8t.chunk_gemm_sr_workspace_size(0, 0, 4, 4, 4, 0) == 0
+
+
 def test_workspace_size_without_a_device(lib):
     """The query plans for the current device; with none it reports 0, and 0
     for invalid arguments."""
@@ -124,6 +151,7 @@ def test_workspace_size_without_a_device(lib):
     assert fp8t.chunk_gemm_workspace_size(0, 0, 128, 128, 1024, 64, 0) == 0
     assert fp8t.chunk_gemm_fp8_workspace_size(0, 0, 128, 128, 1024, 64, 0) == 0
     assert fp8t.chunk_gemm_workspace_size(0, 0, 128, 128, 1024, 0, 0) == 0
+    assert fp8t.chunk_gemm_sr_workspace_size(0, 0, 128, 128, 1024, 64) == 0
 
 
 def test_sr_weight_update_rejects(lib):

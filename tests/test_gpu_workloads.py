@@ -99,6 +99,29 @@ def test_conv_stage_gemms(conv):
     check_gemm_points(Xd, Dd, Xo, Do, K, N, M, 64, 1, 0, 192, 602, "conv wgrad")
 
 
+def test_conv_stage_sr_gemms(conv):
+    """chunk_gemm_sr at the conv-stage shapes, in the launch configuration the
+    benchmark times (workspace from the query), on sampled outputs."""
+    Xd, Xo = quantize_both(conv["Xcol"])
+    Wd, Wo = quantize_both(conv["W"])
+    Dd, Do = quantize_both(conv["dY"], conv["dy_scale"])
+    M, K = conv["Xcol"].shape
+    N = conv["W"].shape[1]
+    for (Ad, Bd, Ao, Bo, m, n, k, ta, tb, npts, what) in (
+            (Xd, Wd, Xo, Wo, M, N, K, 0, 0, 256, "fwd"),
+            (Xd, Dd, Xo, Do, K, N, M, 1, 0, 96, "wgrad")):
+        wb = fp8t.chunk_gemm_sr_workspace_size(ta, tb, m, n, k, 64)
+        ws = torch.empty(wb, dtype=torch.uint8, device=DEV) if wb else None
+        C = torch.empty((m, n), dtype=torch.uint16, device=DEV)
+        say(f"conv {what} chunk_gemm_sr {m}x{n}x{k} ws={wb}")
+        fp8t.chunk_gemm_sr(ta, tb, m, n, k, 64, Ad, Ad.shape[1], Bd, Bd.shape[1], C, n, 17, 0,
+                           ws, wb)
+        r, c = sample_points(m, n, npts, 650 + ta)
+        ref = oracle.chunk_gemm_sr_points(Ao, Bo, 64, r, c, ta, tb, seed=17, offset=0)
+        got = host(C)[r, c]
+        assert np.array_equal(got, ref), (what, np.flatnonzero(got != ref)[:5])
+
+
 @pytest.mark.parametrize("K", workloads.SWEEP_K)
 def test_long_accumulation_sweep(K):
     A32, B32 = workloads.sweep_gemm(K)

@@ -113,7 +113,7 @@ def _uniform(i, j, q, w3, idx, seed):
 @pytest.mark.parametrize("ta,tb", [(0, 0), (1, 1)])
 def test_sr_independent_formulation(ta, tb):
     rng = np.random.default_rng(910 + ta)
-    M, N, K, CL, seed, offset = 3, 2, 19, 4, 77, 5
+    M, N, K, CL, seed, offset = 3, 11, 19, 4, 77, 5
     a = (rng.standard_normal((M, K)) * 8).astype(np.float32)
     b = (rng.standard_normal((K, N)) * 8).astype(np.float32)
     A, B = _q(a.T if ta else a), _q(b.T if tb else b)
@@ -127,9 +127,10 @@ def test_sr_independent_formulation(ta, tb):
                 P = 0.0
                 for k in range(c0, min(K, c0 + CL)):
                     x = np.float32(P) + np.float32(av[i, k] * bv[k, j])
-                    P = _sr_rational(x, _uniform(i, j, k // 8, 2 * offset, k % 8, seed))
+                    P = _sr_rational(x, _uniform(i, j // 4, k // 2, 2 * offset,
+                                                 4 * (k % 2) + j % 4, seed))
                 x = np.float32(S) + np.float32(P)
-                S = _sr_rational(x, _uniform(i, j, c, 2 * offset + 1, 0, seed))
+                S = _sr_rational(x, _uniform(i, j // 8, c, 2 * offset + 1, j % 8, seed))
             assert got[i, j] == S, (i, j, got[i, j], S)
     # and it differs from nearest rounding somewhere (the roundings are live)
     rn = oracle.p16_value(oracle.chunk_gemm(A, B, CL, ta, tb))
