@@ -81,6 +81,16 @@ def fast_peak_mac_s(cl):
     return min(FP8_MFMA_MAC_S, VALU_LANE_OPS * cl / 8.0)
 
 
+def sr_gemm_peak_mac_s():
+    """ALU ceiling of chunk_gemm_sr: per multiply-accumulate one FP32 FMA, the
+    stochastic rounding (an add and an and on the raw bits) and the uniform's
+    extraction (a shift, or a half-rate bit-field extract: 1.5 on average), plus
+    1/8 of a Philox4x32-10 block (20 64-bit multiplies at half rate, 20
+    three-input xors, 4 complements = 64 full-rate slots): 12.5 full-rate VALU
+    slots per MAC."""
+    return VALU_LANE_OPS / 12.5
+
+
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
@@ -145,8 +155,23 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
       result only) against chunk_gemm followed by fp8_quantize of the FP16
       result, both modes;
     * sr_weight_update at a 50-layer residual CNN's 25.6 M parameters
-      (momentum 0.9, weight decay 1e-4, FP8 copy), against HBM."""
+      (momentum 0.9, weight decay 1e-4, FP8 copy), against HBM;
+    * chunk_gemm_sr (stochastic rounding after every FP16 addition) on the
+      forward and weight-gradient shapes, against its ALU ceiling."""
     out = {}
+    sr = {}
+    for name, (ta, tb, m_, n_, k_, A, B) in (("fwd", (0, 0, M, N, K, X8, W8)),
+                                             ("wgrad", (1, 0, K, N, M, X8, D8))):
+        wb = fp8t.chunk_gemm_sr_workspace_size(ta, tb, m_, n_, k_, CL)
+        ws = u8(wb) if wb else None
+        C = u16(m_, n_)
+        t = time_ms(torch, lambda: fp8t.chunk_gemm_sr(ta, tb, m_, n_, k_, CL, A, A.shape[1], B,
+                                                      B.shape[1], C, n_, 7, 0, ws, wb), 2)
+        sr[name] = {"ms": t, "tmac_s": m_ * n_ * k_ / (t * 1e-3) / 1e12,
+                    "frac_of_alu_bound": m_ * n_ * k_ / (t * 1e-3) / sr_gemm_peak_mac_s(),
+                    "workspace_mb": wb / 1e6}
+        del ws, C
+    out["sr_gemm"] = sr
     C16, C8 = u16(M, K), u8(M, K)
     for mode, tag in ((fp8t.EXACT, "exact"), (fp8t.FAST, "fast")):
         wb = fp8t.chunk_gemm_fp8_workspace_size(0, 1, M, K, N, CL, mode)

@@ -78,6 +78,11 @@ def lib():
                                                vp, vp, i64, vp]
         L.cpu_sr_weight_update.restype = ctypes.c_int
         L.cpu_sr_weight_update.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, u64, u64]
+        L.cpu_adam_update.restype = ctypes.c_int
+        L.cpu_adam_update.argtypes = [vp, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, u64,
+                                      u64, u64]
+        L.orc_adam_step_size.restype = f32
+        L.orc_adam_step_size.argtypes = [f32, f32, f32, u64]
         L.orc_num_threads.restype = ctypes.c_int
         L.orc_num_threads.argtypes = []
         _lib = L
@@ -253,6 +258,25 @@ def sr_weight_update(w, g, v=None, *, lr, momentum=0.0, weight_decay=0.0,
                                       float(lr), float(momentum), float(weight_decay),
                                       int(seed), int(offset)), "sr_weight_update")
     return w, v, w8
+
+
+def adam_update(w, g, m, v, *, lr, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0,
+                t=1, seed=0, offset=0, want_w8=True):
+    """Returns (w', m', v', w8 or None); inputs are not modified."""
+    w = np.array(w, dtype=np.uint16, copy=True)
+    g = np.ascontiguousarray(g, dtype=np.uint16)
+    m = np.array(m, dtype=np.uint16, copy=True)
+    v = np.array(v, dtype=np.uint16, copy=True)
+    w8 = np.zeros(w.shape, dtype=np.uint8) if want_w8 else None
+    _check(lib().cpu_adam_update(_ptr(w), _ptr(g), _ptr(m), _ptr(v), _ptr(w8), w.size,
+                                 float(lr), float(beta1), float(beta2), float(eps),
+                                 float(weight_decay), int(t), int(seed), int(offset)),
+           "adam_update")
+    return w, m, v, w8
+
+
+def adam_step_size(lr, beta1, beta2, t):
+    return float(lib().orc_adam_step_size(float(lr), float(beta1), float(beta2), int(t)))
 
 
 def num_threads():

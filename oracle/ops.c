@@ -291,3 +291,85 @@ int cpu_sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v,
     }
     return ORC_OK;
 }
+
+/* ---- ADAM weight update in P16 with stochastic rounding -------------------
+ * Sec. 4 also trains with the ADAM optimizer (Kingma & Ba) using FP8 GEMMs
+ * and FP16 weight updates.  Read here as the SGD update above with ADAM's
+ * moment estimates: every AXPY is formed in FP32 and stochastically rounded
+ * into P16 (Eq. (1)), the moments are P16 buffers like the momentum buffer.
+ * For element i (all FP32 operations IEEE round-to-nearest; sqrtf and the
+ * division correctly rounded):
+ *     g' = SR16(fmaf(wd, w, g))
+ *     m' = SR16(fmaf(beta1, m, (1 - beta1) * g'))
+ *     v' = SR16(fmaf(beta2, v, (1 - beta2) * (g' * g')))
+ *     w' = SR16(fmaf(-alpha_t, m' / (sqrtf(v') + eps), w))
+ *     w8 = Q8(w')
+ * with 1 - beta1 and 1 - beta2 single FP32 subtractions, and the
+ * bias-corrected step size of Kingma & Ba's efficient form,
+ *     alpha_t = lr * sqrt(1 - beta2^t) / (1 - beta1^t),
+ * evaluated in double precision (beta^t by binary exponentiation of the
+ * double value of beta, t >= 1) and rounded once to FP32.
+ * Random bits: one Philox4x32-10 block per element pair (key = seed,
+ * counter = (pair index, offset)), eight 16-bit uniforms (low half first);
+ * element i takes uniforms 4 (i mod 2) + 0, 1, 2, 3 for g', m', v', w'. */
+static double pow_binary(double b, uint64_t t) {
+    double r = 1.0;
+    while (t) {
+        if (t & 1) r *= b;
+        b *= b;
+        t >>= 1;
+    }
+    return r;
+}
+
+float orc_adam_step_size(float lr, float beta1, float beta2, uint64_t t) {
+    const double b1t = pow_binary((double)beta1, t), b2t = pow_binary((double)beta2, t);
+    return (float)((double)lr * sqrt(1.0 - b2t) / (1.0 - b1t));
+}
+
+int cpu_adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,
+                    uint8_t* w8, int64_t n, float lr, float beta1, float beta2,
+                    float eps, float weight_decay, uint64_t t, uint64_t seed,
+                    uint64_t offset) {
+    if (n < 0 || t < 1) return ORC_EINVAL;
+    if (n > 0 && (!w || !g || !m || !v)) return ORC_EINVAL;
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    const float alpha = orc_adam_step_size(lr, beta1, beta2, t);
+    const float c1 = 1.0f - beta1, c2 = 1.0f - beta2;
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++) {
+        uint64_t pair = (uint64_t)i >> 1;
+        const uint32_t ctr[4] = {(uint32_t)pair, (uint32_t)(pair >> 32),
+                                 (uint32_t)offset, (uint32_t)(offset >> 32)};
+        uint32_t words[4];
+        orc_philox4x32_10(ctr, key, words);
+        uint32_t u[8];
+        for (int q = 0; q < 4; q++) {
+            u[2 * q] = words[q] & 0xFFFFu;
+            u[2 * q + 1] = words[q] >> 16;
+        }
+        const uint32_t* h = u + 4 * (i & 1);
+
+        volatile float wf = (float)orc_p16_value(w[i]);
+        volatile float gf = (float)orc_p16_value(g[i]);
+        volatile float mf = (float)orc_p16_value(m[i]);
+        volatile float vf = (float)orc_p16_value(v[i]);
+        uint16_t g1 = orc_sr16(fmaf(weight_decay, wf, gf), h[0]);
+        volatile float g1f = (float)orc_p16_value(g1);
+        volatile float mg = c1 * g1f;
+        uint16_t m1 = orc_sr16(fmaf(beta1, mf, mg), h[1]);
+        volatile float sq = g1f * g1f;
+        volatile float vg = c2 * sq;
+        uint16_t v1 = orc_sr16(fmaf(beta2, vf, vg), h[2]);
+        volatile float m1f = (float)orc_p16_value(m1);
+        volatile float v1f = (float)orc_p16_value(v1);
+        volatile float den = sqrtf(v1f) + eps;
+        volatile float q = m1f / den;
+        uint16_t w1 = orc_sr16(fmaf(-alpha, q, wf), h[3]);
+        w[i] = w1;
+        m[i] = m1;
+        v[i] = v1;
+        if (w8) w8[i] = orc_q8(orc_p16_value(w1));
+    }
+    return ORC_OK;
+}

@@ -83,6 +83,15 @@ int cpu_sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v,
                          uint8_t* w8, int64_t n, float lr, float momentum,
                          float weight_decay, uint64_t seed, uint64_t offset);
 
+/* ADAM step in P16 with stochastic rounding (Sec. 4, Kingma & Ba), defined
+ * in ops.c; m and v are the P16 moment buffers, updated in place; t >= 1 is
+ * the step number.  orc_adam_step_size is its bias-corrected step size. */
+int cpu_adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,
+                    uint8_t* w8, int64_t n, float lr, float beta1, float beta2,
+                    float eps, float weight_decay, uint64_t t, uint64_t seed,
+                    uint64_t offset);
+float orc_adam_step_size(float lr, float beta1, float beta2, uint64_t t);
+
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int orc_num_threads(void);
 
