@@ -157,7 +157,8 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
     * sr_weight_update at a 50-layer residual CNN's 25.6 M parameters
       (momentum 0.9, weight decay 1e-4, FP8 copy), against HBM;
     * chunk_gemm_sr (stochastic rounding after every FP16 addition) on the
-      forward and weight-gradient shapes, against its ALU ceiling."""
+      forward and weight-gradient shapes, against its ALU ceiling;
+    * adam_update at 25.6 M parameters, against HBM."""
     out = {}
     sr = {}
     for name, (ta, tb, m_, n_, k_, A, B) in (("fwd", (0, 0, M, N, K, X8, W8)),
@@ -200,6 +201,14 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
     t = time_ms(torch, upd, 20)
     out["sr_update_25_6M"] = {"us": t * 1e3, "gb_s": 11 * n / (t * 1e-3) / 1e9,
                               "frac_of_hbm": 11 * n / (t * 1e-3) / HBM_BYTES_S}
+    # ADAM: read w, g, m, v (8 B), write w, m, v (6 B) and w8 (1 B) per parameter
+    m16, s16 = u16(n), u16(n)
+    fp8t.fp16_quantize(torch.randn(n, device="cuda", generator=g) * 1e-4, m16)
+    fp8t.fp16_quantize(torch.randn(n, device="cuda", generator=g).abs() * 1e-6, s16)
+    t = time_ms(torch, lambda: fp8t.adam_update(w16, g16, m16, s16, w8, n, 1e-3, 0.9, 0.999,
+                                                 1e-8, 1e-4, 10, 7, 0), 20)
+    out["adam_update_25_6M"] = {"us": t * 1e3, "gb_s": 15 * n / (t * 1e-3) / 1e9,
+                                "frac_of_hbm": 15 * n / (t * 1e-3) / HBM_BYTES_S}
     return out
 
 

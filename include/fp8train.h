@@ -231,6 +231,37 @@ int sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v, uint8_t* w8,
                      int64_t n, float lr, float momentum, float weight_decay,
                      uint64_t seed, uint64_t offset, hipStream_t stream);
 
+/*
+ * adam_update -- one ADAM step (Kingma & Ba; Sec. 4 trains with ADAM using
+ * FP8 GEMMs and FP16 weight updates) with every AXPY stochastically rounded
+ * into FP16 as in sr_weight_update, keeping FP16 master weights and moment
+ * buffers and writing the FP8 weight copy.
+ *
+ * For i in [0, n) (every FP32 operation IEEE round-to-nearest; the square
+ * root and the division correctly rounded; SR as in sr_weight_update):
+ *   g' = SR(fmaf(weight_decay, w[i], g[i]))
+ *   m' = SR(fmaf(beta1, m[i], (1 - beta1) * g'))
+ *   v' = SR(fmaf(beta2, v[i], (1 - beta2) * (g' * g')))
+ *   w' = SR(fmaf(-alpha_t, m' / (sqrtf(v') + eps), w[i]))
+ *   w[i] = w', m[i] = m', v[i] = v', w8[i] = FP8 of w'
+ * 1 - beta1, 1 - beta2 are FP32 subtractions.  alpha_t = lr sqrt(1 - beta2^t)
+ * / (1 - beta1^t) is evaluated in double precision (beta^t by binary
+ * exponentiation of the double value of beta) and rounded once to float;
+ * t >= 1 is the step number.  Uniforms: one Philox4x32-10 block per element
+ * pair, key = seed, counter = (i/2 low, i/2 high, offset low, offset high),
+ * eight 16-bit uniforms (low half first); element i uses uniforms
+ * 4*(i%2) + 0, 1, 2, 3 for g', m', v', w'.
+ *
+ * w, g, m, v: FP16 codes [n] (w, m, v updated in place); w8: FP8 codes [n]
+ * or NULL.  w8 must not overlap the others.
+ * Errors: FP8T_EINVAL (n < 0, t < 1, a NULL w, g, m or v with n > 0);
+ * FP8T_EHIP.
+ */
+int adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,
+                uint8_t* w8, int64_t n, float lr, float beta1, float beta2,
+                float eps, float weight_decay, uint64_t t, uint64_t seed,
+                uint64_t offset, hipStream_t stream);
+
 /* A static, human-readable description of a status code. */
 const char* fp8t_status_string(int status);
 

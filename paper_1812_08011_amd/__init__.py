@@ -55,6 +55,9 @@ def lib():
                                     u64, u64, vp, sz, vp]
         L.chunk_gemm_sr_workspace_size.restype = sz
         L.chunk_gemm_sr_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64]
+        L.adam_update.restype = i32
+        L.adam_update.argtypes = [vp, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, u64, u64,
+                                  u64, vp]
         L.sr_weight_update.restype = i32
         L.sr_weight_update.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, u64, u64, vp]
         L.fp8t_status_string.restype = ctypes.c_char_p
@@ -176,4 +179,14 @@ def sr_weight_update(w, g, v, w8, n, lr, momentum, weight_decay, seed, offset, s
            lib().sr_weight_update(_ptr(w), _ptr(g), _ptr(v), _ptr(w8), int(n), float(lr),
                                   float(momentum), float(weight_decay), int(seed), int(offset),
                                   _stream(stream)))
+    return w
+
+
+def adam_update(w, g, m, v, w8, n, lr, beta1, beta2, eps, weight_decay, t, seed, offset,
+                stream=None):
+    """The C-ABI call with the same argument order; w8 may be None."""
+    _check("adam_update",
+           lib().adam_update(_ptr(w), _ptr(g), _ptr(m), _ptr(v), _ptr(w8), int(n), float(lr),
+                             float(beta1), float(beta2), float(eps), float(weight_decay), int(t),
+                             int(seed), int(offset), _stream(stream)))
     return w

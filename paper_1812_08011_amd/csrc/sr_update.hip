@@ -233,6 +233,98 @@ __global__ __launch_bounds__(kThreads) void sr_update_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// ADAM (Kingma & Ba) with the same FP16 stochastic-rounding AXPYs
+// ---------------------------------------------------------------------------
+
+struct adam_params {
+    float alpha;              // bias-corrected step size
+    float beta1, beta2, c1, c2, eps, weight_decay;
+    uint32_t k0, k1, off_lo, off_hi;
+};
+
+// One element with uniforms h[0..3]; IEEE round-to-nearest for every FP32
+// operation (the division and square root correctly rounded).
+__device__ __forceinline__ void adam_one(uint32_t wc, uint32_t gc, uint32_t mc, uint32_t vc,
+                                         const uint32_t (&h)[4], const adam_params& p,
+                                         uint16_t& w_out, uint16_t& m_out, uint16_t& v_out,
+                                         uint32_t& w8_out) {
+    const float w = fp16_to_f32(wc), g = fp16_to_f32(gc);
+    const float m = fp16_to_f32(mc), v = fp16_to_f32(vc);
+    const sr_result g1 = sr16(__builtin_fmaf(p.weight_decay, w, g), h[0]);
+    const sr_result m1 = sr16(__builtin_fmaf(p.beta1, m, __fmul_rn(p.c1, g1.value)), h[1]);
+    const sr_result v1 =
+        sr16(__builtin_fmaf(p.beta2, v, __fmul_rn(p.c2, __fmul_rn(g1.value, g1.value))), h[2]);
+    // sqrtf and / are correctly rounded (hipcc default for FP32; the
+    // __fsqrt_rn intrinsic maps to the approximate hardware square root)
+    const float q = m1.value / __fadd_rn(__builtin_sqrtf(v1.value), p.eps);
+    const sr_result w1 = sr16(__builtin_fmaf(-p.alpha, q, w), h[3]);
+    w_out = w1.code;
+    m_out = m1.code;
+    v_out = v1.code;
+    w8_out = f32_to_fp8(w1.value);
+}
+
+// One thread per element pair (one Philox block: element 2 pr takes uniforms
+// 0..3, element 2 pr + 1 uniforms 4..7); 4-byte accesses of w, g, m, v when
+// the pointers allow them.
+__global__ __launch_bounds__(kThreads) void adam_update_kernel(
+    uint16_t* __restrict__ w, const uint16_t* __restrict__ g, uint16_t* __restrict__ m,
+    uint16_t* __restrict__ v, uint8_t* __restrict__ w8, int64_t n, adam_params p, int vec_ok) {
+    const int64_t npairs = (n + 1) / 2;
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t pr = (int64_t)blockIdx.x * kThreads + threadIdx.x; pr < npairs; pr += stride) {
+        const u32x4 ctr = {(uint32_t)pr, (uint32_t)((uint64_t)pr >> 32), p.off_lo, p.off_hi};
+        const u32x4 r = philox4x32_10(ctr, p.k0, p.k1);
+        const uint32_t h0[4] = {r.x & 0xFFFFu, r.x >> 16, r.y & 0xFFFFu, r.y >> 16};
+        const uint32_t h1[4] = {r.z & 0xFFFFu, r.z >> 16, r.w & 0xFFFFu, r.w >> 16};
+        const int64_t i = 2 * pr;
+        const bool both = i + 1 < n;
+        uint32_t wp, gp, mp, vp;
+        if (both && vec_ok) {
+            wp = reinterpret_cast<const uint32_t*>(w)[pr];
+            gp = reinterpret_cast<const uint32_t*>(g)[pr];
+            mp = reinterpret_cast<const uint32_t*>(m)[pr];
+            vp = reinterpret_cast<const uint32_t*>(v)[pr];
+        } else {
+            wp = w[i] | (both ? (uint32_t)w[i + 1] << 16 : 0u);
+            gp = g[i] | (both ? (uint32_t)g[i + 1] << 16 : 0u);
+            mp = m[i] | (both ? (uint32_t)m[i + 1] << 16 : 0u);
+            vp = v[i] | (both ? (uint32_t)v[i + 1] << 16 : 0u);
+        }
+        uint16_t wo[2], mo[2], vo[2];
+        uint32_t q8[2];
+        adam_one(wp & 0xFFFFu, gp & 0xFFFFu, mp & 0xFFFFu, vp & 0xFFFFu, h0, p, wo[0], mo[0],
+                 vo[0], q8[0]);
+        adam_one(wp >> 16, gp >> 16, mp >> 16, vp >> 16, h1, p, wo[1], mo[1], vo[1], q8[1]);
+        if (both && vec_ok) {
+            reinterpret_cast<uint32_t*>(w)[pr] = wo[0] | ((uint32_t)wo[1] << 16);
+            reinterpret_cast<uint32_t*>(m)[pr] = mo[0] | ((uint32_t)mo[1] << 16);
+            reinterpret_cast<uint32_t*>(v)[pr] = vo[0] | ((uint32_t)vo[1] << 16);
+            if (w8) reinterpret_cast<uint16_t*>(w8)[pr] = (uint16_t)(q8[0] | (q8[1] << 8));
+        } else {
+            for (int e = 0; e < (both ? 2 : 1); ++e) {
+                w[i + e] = wo[e];
+                m[i + e] = mo[e];
+                v[i + e] = vo[e];
+                if (w8) w8[i + e] = (uint8_t)q8[e];
+            }
+        }
+    }
+}
+
+// Bias-corrected step size lr sqrt(1 - beta2^t) / (1 - beta1^t) in double
+// precision, beta^t by binary exponentiation, rounded once to float.
+double pow_binary(double b, uint64_t t) {
+    double r = 1.0;
+    while (t) {
+        if (t & 1) r *= b;
+        b *= b;
+        t >>= 1;
+    }
+    return r;
+}
+
 }  // namespace
 }  // namespace fp8t
 
@@ -276,5 +368,35 @@ extern "C" int sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v, uin
     else if (w8) { FP8T_LAUNCH(false, true); }
     else { FP8T_LAUNCH(false, false); }
 #undef FP8T_LAUNCH
+    return launch_status();
+}
+
+extern "C" int adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,
+                           uint8_t* w8, int64_t n, float lr, float beta1, float beta2, float eps,
+                           float weight_decay, uint64_t t, uint64_t seed, uint64_t offset,
+                           hipStream_t stream) {
+    if (n < 0 || t < 1) return FP8T_EINVAL;
+    if (n == 0) return FP8T_OK;
+    if (!w || !g || !m || !v) return FP8T_EINVAL;
+    adam_params p;
+    const double b1t = pow_binary((double)beta1, t), b2t = pow_binary((double)beta2, t);
+    p.alpha = (float)((double)lr * std::sqrt(1.0 - b2t) / (1.0 - b1t));
+    p.beta1 = beta1;
+    p.beta2 = beta2;
+    p.c1 = 1.0f - beta1;
+    p.c2 = 1.0f - beta2;
+    p.eps = eps;
+    p.weight_decay = weight_decay;
+    p.k0 = (uint32_t)seed;
+    p.k1 = (uint32_t)(seed >> 32);
+    p.off_lo = (uint32_t)offset;
+    p.off_hi = (uint32_t)(offset >> 32);
+    const int vec_ok = aligned(w, 4) && aligned(g, 4) && aligned(m, 4) && aligned(v, 4) &&
+                       (!w8 || aligned(w8, 2));
+    const int64_t npairs = (n + 1) / 2;
+    int64_t groups = (npairs + kThreads - 1) / kThreads;
+    if (groups > 256 * 32) groups = 256 * 32;
+    hipLaunchKernelGGL(adam_update_kernel, dim3((unsigned)groups), dim3(kThreads), 0, stream, w,
+                       g, m, v, w8, n, p, vec_ok);
     return launch_status();
 }

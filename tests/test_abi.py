@@ -34,7 +34,7 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "fp8_quantize", "fp16_quantize", "chunk_gemm", "chunk_gemm_workspace_size",
         "chunk_gemm_fp8", "chunk_gemm_fp8_workspace_size",
-        "chunk_gemm_sr", "chunk_gemm_sr_workspace_size",
+        "chunk_gemm_sr", "chunk_gemm_sr_workspace_size", "adam_update",
         "sr_weight_update", "fp8t_status_string"])
 
 
@@ -162,6 +162,19 @@ def test_sr_weight_update_rejects(lib):
     assert f(None, FAKE, None, None, 10, 0.1, 0.0, 0.0, 1, 0, None) == E
     assert f(FAKE, None, None, None, 10, 0.1, 0.0, 0.0, 1, 0, None) == E
     assert f(None, None, None, None, 0, 0.1, 0.0, 0.0, 1, 0, None) == fp8t.OK
+
+
+def test_adam_update_rejects(lib):
+    E = fp8t.EINVAL
+    f = lib.adam_update
+    args = [FAKE, FAKE, FAKE, FAKE, None, 10, 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 1, 0, None]
+    assert f(*args[:11], 0, *args[12:]) == E                  # t = 0
+    assert f(*args[:5], -1, *args[6:]) == E                   # n < 0
+    for k in range(4):                                        # NULL w, g, m, v
+        a = list(args)
+        a[k] = None
+        assert f(*a) == E
+    assert f(None, None, None, None, None, 0, *args[6:]) == fp8t.OK
 
 
 def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
