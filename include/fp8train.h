@@ -201,6 +201,32 @@ size_t chunk_gemm_sr_workspace_size(int trans_a, int trans_b, int64_t M,
                                     int64_t N, int64_t K, int64_t CL);
 
 /*
+ * chunk_gemm_p16 -- the GEMM with FP16 operands that Sec. 3 keeps for the last
+ * layer of a network (Forward, Backward and Gradient GEMMs alike).  As
+ * chunk_gemm's exact mode with FP16 codes as operands, the multiplication
+ * also done in FP16 (Fig. 3(a) with FP_mult = FP_acc = FP16):
+ *   within chunk c (ascending k):  P = RN(P + RN(a(k) * b(k)))
+ *   after chunk c:                 S = RN(S + P)
+ * RN = round to the nearest FP16 value (ties to even) of the exact value;
+ * P, S start at +0; C(i, j) = the FP16 code of S (+0 when K == 0).
+ * Bit-exact.  A, B: FP16 codes (uint16_t) in the layouts of chunk_gemm; C,
+ * CL and the workspace contract as chunk_gemm (query:
+ * chunk_gemm_p16_workspace_size).  Errors: as chunk_gemm.
+ */
+int chunk_gemm_p16(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                   int64_t CL, const uint16_t* A, int64_t lda, const uint16_t* B,
+                   int64_t ldb, uint16_t* C, int64_t ldc, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * chunk_gemm_p16_workspace_size -- bytes of workspace the fastest plan of
+ * chunk_gemm_p16 needs on the current device (0 if none, or for invalid
+ * arguments).
+ */
+size_t chunk_gemm_p16_workspace_size(int trans_a, int trans_b, int64_t M,
+                                     int64_t N, int64_t K, int64_t CL);
+
+/*
  * sr_weight_update -- one SGD step entirely in FP16 with floating-point
  * stochastic rounding (Sec. 2.2 / Fig. 2(b): L2-Reg, Momentum-Acc and
  * Weight-Upd AXPYs; Sec. 2.3 Eq. (1); Sec. 4.3), keeping the FP16 master

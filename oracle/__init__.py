@@ -78,6 +78,12 @@ def lib():
                                                vp, vp, i64, vp]
         L.cpu_sr_weight_update.restype = ctypes.c_int
         L.cpu_sr_weight_update.argtypes = [vp, vp, vp, vp, i64, f32, f32, f32, u64, u64]
+        L.cpu_chunk_gemm_p16.restype = ctypes.c_int
+        L.cpu_chunk_gemm_p16.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64, i64,
+                                         vp, i64, vp, i64, vp, i64]
+        L.cpu_chunk_gemm_p16_points.restype = ctypes.c_int
+        L.cpu_chunk_gemm_p16_points.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64,
+                                                i64, vp, i64, vp, i64, vp, vp, i64, vp]
         L.cpu_adam_update.restype = ctypes.c_int
         L.cpu_adam_update.argtypes = [vp, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, u64,
                                       u64, u64]
@@ -244,6 +250,35 @@ def chunk_gemm_sr_points(A, B, CL, rows, cols, trans_a=0, trans_b=0, *, seed, of
                                           _ptr(A), lda, _ptr(B), ldb, int(seed), int(offset),
                                           _ptr(rows), _ptr(cols), rows.size, _ptr(out)),
            "chunk_gemm_sr_points")
+    return out
+
+
+def chunk_gemm_p16(A, B, CL, trans_a=0, trans_b=0):
+    """C = op(A) op(B) with P16 operands (uint16 codes): products rounded to
+    P16, chunk-based P16 accumulation."""
+    A = np.ascontiguousarray(A, dtype=np.uint16)
+    B = np.ascontiguousarray(B, dtype=np.uint16)
+    M, N, K = _gemm_dims(trans_a, trans_b, A, B)
+    C = np.zeros((M, N), dtype=np.uint16)
+    lda = A.shape[1] if A.shape[1] > 0 else 1
+    ldb = B.shape[1] if B.shape[1] > 0 else 1
+    _check(lib().cpu_chunk_gemm_p16(int(trans_a), int(trans_b), M, N, K, int(CL), _ptr(A), lda,
+                                    _ptr(B), ldb, _ptr(C), max(N, 1)), "chunk_gemm_p16")
+    return C
+
+
+def chunk_gemm_p16_points(A, B, CL, rows, cols, trans_a=0, trans_b=0):
+    A = np.ascontiguousarray(A, dtype=np.uint16)
+    B = np.ascontiguousarray(B, dtype=np.uint16)
+    M, N, K = _gemm_dims(trans_a, trans_b, A, B)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    out = np.zeros(rows.size, dtype=np.uint16)
+    lda = A.shape[1] if A.shape[1] > 0 else 1
+    ldb = B.shape[1] if B.shape[1] > 0 else 1
+    _check(lib().cpu_chunk_gemm_p16_points(int(trans_a), int(trans_b), M, N, K, int(CL),
+                                           _ptr(A), lda, _ptr(B), ldb, _ptr(rows), _ptr(cols),
+                                           rows.size, _ptr(out)), "chunk_gemm_p16_points")
     return out
 
 

@@ -240,6 +240,76 @@ int cpu_chunk_gemm_sr_points(int trans_a, int trans_b, int64_t M, int64_t N,
     return ORC_OK;
 }
 
+/* ---- chunk-based GEMM with P16 operands ------------------------------------
+ * Sec. 3 keeps the last layer's GEMMs in FP16.  Read as Fig. 3(a) with
+ * FP_mult = FP_acc = P16: each product of two P16 operands is rounded to P16
+ * (nearest even; the multiplication happens in FP_mult), then the products are
+ * accumulated exactly as in chunk_gemm's exact mode:
+ *     P = RN16(P + RN16(a(i,k) b(k,j)))   within a chunk, ascending k
+ *     S = RN16(S + P)                      after each chunk
+ * The product of two P16 values (at most 20 significant bits, magnitude
+ * 2^-78 .. 2^64) is exact in double precision. */
+static inline uint16_t op16(int trans, const uint16_t* X, int64_t ld, int64_t r, int64_t c) {
+    return trans ? X[c * ld + r] : X[r * ld + c];
+}
+
+static uint16_t chunk_dot_p16(int trans_a, int trans_b, int64_t K, int64_t CL,
+                              const uint16_t* A, int64_t lda, const uint16_t* B,
+                              int64_t ldb, int64_t i, int64_t j) {
+    uint16_t S = 0;
+    for (int64_t c0 = 0; c0 < K; c0 += CL) {
+        int64_t c1 = (K - c0 < CL) ? K : c0 + CL;
+        uint16_t P = 0;
+        for (int64_t k = c0; k < c1; k++) {
+            const double a = orc_p16_value(op16(trans_a, A, lda, i, k));
+            const double b = orc_p16_value(op16(trans_b, B, ldb, k, j));
+            P = orc_add16(P, orc_rn16(a * b));
+        }
+        S = orc_add16(S, P);
+    }
+    return S;
+}
+
+static int p16_args_ok(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                       int64_t CL, const uint16_t* A, int64_t lda, const uint16_t* B,
+                       int64_t ldb) {
+    if (M < 0 || N < 0 || K < 0 || CL < 1) return 0;
+    if ((trans_a != 0 && trans_a != 1) || (trans_b != 0 && trans_b != 1)) return 0;
+    if (M > 0 && N > 0 && K > 0) {
+        if (!A || !B) return 0;
+        if (lda < (trans_a ? M : K)) return 0;
+        if (ldb < (trans_b ? K : N)) return 0;
+    }
+    return 1;
+}
+
+int cpu_chunk_gemm_p16(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                       int64_t CL, const uint16_t* A, int64_t lda,
+                       const uint16_t* B, int64_t ldb, uint16_t* C, int64_t ldc) {
+    if (!p16_args_ok(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb)) return ORC_EINVAL;
+    if (M > 0 && N > 0 && (!C || ldc < N)) return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t i = 0; i < M; i++)
+        for (int64_t j = 0; j < N; j++)
+            C[i * ldc + j] = chunk_dot_p16(trans_a, trans_b, K, CL, A, lda, B, ldb, i, j);
+    return ORC_OK;
+}
+
+int cpu_chunk_gemm_p16_points(int trans_a, int trans_b, int64_t M, int64_t N,
+                              int64_t K, int64_t CL, const uint16_t* A, int64_t lda,
+                              const uint16_t* B, int64_t ldb, const int64_t* rows,
+                              const int64_t* cols, int64_t npts, uint16_t* out) {
+    if (!p16_args_ok(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb)) return ORC_EINVAL;
+    if (npts < 0 || (npts > 0 && (!rows || !cols || !out))) return ORC_EINVAL;
+    for (int64_t p = 0; p < npts; p++)
+        if (rows[p] < 0 || rows[p] >= M || cols[p] < 0 || cols[p] >= N)
+            return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t p = 0; p < npts; p++)
+        out[p] = chunk_dot_p16(trans_a, trans_b, K, CL, A, lda, B, ldb, rows[p], cols[p]);
+    return ORC_OK;
+}
+
 /* ---- SGD weight update in P16 with stochastic rounding -------------------
  * Sec. 2.2 (Fig. 2(b)) and Sec. 4.3: the three AXPYs of an SGD step --
  * L2 regularisation, momentum accumulation and the weight update -- all run

@@ -79,6 +79,16 @@ int cpu_chunk_gemm_sr_points(int trans_a, int trans_b, int64_t M, int64_t N,
                              uint32_t offset, const int64_t* rows,
                              const int64_t* cols, int64_t npts, uint16_t* out);
 
+/* chunk_gemm with P16 operands (the last layer's GEMMs, Sec. 3): products
+ * rounded to P16, then exact-mode chunked accumulation (ops.c). */
+int cpu_chunk_gemm_p16(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                       int64_t CL, const uint16_t* A, int64_t lda,
+                       const uint16_t* B, int64_t ldb, uint16_t* C, int64_t ldc);
+int cpu_chunk_gemm_p16_points(int trans_a, int trans_b, int64_t M, int64_t N,
+                              int64_t K, int64_t CL, const uint16_t* A, int64_t lda,
+                              const uint16_t* B, int64_t ldb, const int64_t* rows,
+                              const int64_t* cols, int64_t npts, uint16_t* out);
+
 int cpu_sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v,
                          uint8_t* w8, int64_t n, float lr, float momentum,
                          float weight_decay, uint64_t seed, uint64_t offset);

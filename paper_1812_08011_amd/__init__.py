@@ -55,6 +55,11 @@ def lib():
                                     u64, u64, vp, sz, vp]
         L.chunk_gemm_sr_workspace_size.restype = sz
         L.chunk_gemm_sr_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64]
+        L.chunk_gemm_p16.restype = i32
+        L.chunk_gemm_p16.argtypes = [i32, i32, i64, i64, i64, i64, vp, i64, vp, i64, vp, i64,
+                                     vp, sz, vp]
+        L.chunk_gemm_p16_workspace_size.restype = sz
+        L.chunk_gemm_p16_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64]
         L.adam_update.restype = i32
         L.adam_update.argtypes = [vp, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, u64, u64,
                                   u64, vp]
@@ -190,3 +195,18 @@ def adam_update(w, g, m, v, w8, n, lr, beta1, beta2, eps, weight_decay, t, seed,
                              float(beta1), float(beta2), float(eps), float(weight_decay), int(t),
                              int(seed), int(offset), _stream(stream)))
     return w
+
+
+def chunk_gemm_p16_workspace_size(trans_a, trans_b, M, N, K, CL):
+    return int(lib().chunk_gemm_p16_workspace_size(int(trans_a), int(trans_b), int(M), int(N),
+                                                   int(K), int(CL)))
+
+
+def chunk_gemm_p16(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, workspace=None,
+                   workspace_bytes=0, stream=None):
+    """The C-ABI call with the same argument order (FP16-code operands)."""
+    _check("chunk_gemm_p16",
+           lib().chunk_gemm_p16(int(trans_a), int(trans_b), int(M), int(N), int(K), int(CL),
+                                _ptr(A), int(lda), _ptr(B), int(ldb), _ptr(C), int(ldc),
+                                _ptr(workspace), int(workspace_bytes), _stream(stream)))
+    return C

@@ -1,32 +1,43 @@
-// chunk_gemm_sr: the chunk-based FP8 GEMM of Sec. 2.3 / Fig. 3(a) with every
-// FP16 addition rounded stochastically (Eq. (1)) instead of to nearest -- the
-// paper's second rounding mode after FP16 additions, whose behaviour on long
-// accumulations Fig. 3(b) compares with nearest rounding.
+// Vector-ALU tile kernel for two variants of the chunk-based GEMM of
+// Sec. 2.3 / Fig. 3(a):
+//
+// * chunk_gemm_sr -- FP8 operands, every FP16 addition rounded stochastically
+//   (Eq. (1)) instead of to nearest: the paper's second rounding mode after
+//   FP16 additions, whose behaviour on long accumulations Fig. 3(b) compares
+//   with nearest rounding;
+// * chunk_gemm_p16 -- FP16 operands (the last layer's GEMMs, which Sec. 3
+//   keeps in FP16): each product is rounded to FP16 (the multiplication in
+//   FP_mult = FP16 of Fig. 3(a)), then accumulated in chunks with rounding to
+//   nearest, as in chunk_gemm's exact mode.
 //
 // Each addition first forms the FP32 sum of the running value and the next
-// term (the product of two FP8 values is exact in FP32) and then rounds it
-// into FP16 with a 16-bit uniform.  As in the exact mode, FP16 quantities are
-// held scaled by 2^96 (fp8t_device.h), so FP16 overflow is FP32 overflow and
-// FP16 subnormals are FP32 normals.  There, stochastic rounding of the 14
-// discarded mantissa bits D with uniform u rounds the magnitude up iff
+// term (products of two FP8 values are exact in FP32; products of two FP16
+// values, 20 significant bits, too) and then rounds it into FP16.  As in the
+// exact mode, FP16 quantities are held scaled by 2^96 (fp8t_device.h), so FP16
+// overflow is FP32 overflow and FP16 subnormals are FP32 normals: FP8 operands
+// enter as a(k) 2^96 and b(k), FP16 operands as a(k) 2^48 and b(k) 2^48.
+// Rounding to nearest is rn16s on the raw bits.  Stochastic rounding of the
+// 14 discarded mantissa bits D with uniform u rounds the magnitude up iff
 // D > (u >> 2); adding (2^14 - 1 - (u >> 2)) to the raw bits and clearing the
 // low 14 bits does exactly that, with the carry running into the exponent
 // (and to the Inf encoding past the largest FP16 value).  Sums below 2^-30
 // are multiples of 2^-39 with at most 9 significant bits, so their discarded
-// bits are zero and no rounding happens, as Eq. (1)'s fixed subnormal step
-// requires.
+// bits are zero and neither rounding changes them, as the fixed subnormal
+// step requires.  A product of FP16 values below 2^-30 is rounded to a
+// multiple of 2^-39 by adding and subtracting 1.5 x 2^-16 (2^80 scaled).
 //
-// Random bits: Philox4x32-10, key = seed, eight 16-bit uniforms per block
-// (word halves, low half first).  The addition of product k into output
-// (i, j) takes uniform 4 (k mod 2) + (j mod 4) of block (i, j / 4, k / 2,
-// 2 offset): a thread owning 4 x 4 outputs (four rows of four aligned
-// columns) draws four blocks per two k.  The addition of chunk c into the
-// running sum takes uniform j mod 8 of block (i, j / 8, c, 2 offset + 1).
+// Random bits (chunk_gemm_sr): Philox4x32-10, key = seed, eight 16-bit
+// uniforms per block (word halves, low half first).  The addition of product
+// k into output (i, j) takes uniform 4 (k mod 2) + (j mod 4) of block
+// (i, j / 4, k / 2, 2 offset): a thread owning 4 x 4 outputs (four rows of
+// four aligned columns) draws four blocks per two k.  The addition of chunk c
+// into the running sum takes uniform j mod 8 of block (i, j / 8, c,
+// 2 offset + 1).
 //
 // The work decomposition is the persistent plan of gemm_plan.h: whole tiles,
 // then the chunks of the remaining tiles shared out as ranges; a piece that
 // does not start at chunk 0 leaves each chunk's FP16 sum in the workspace and
-// chunk_fold_sr continues the running sum over them in ascending order, with
+// chunk_fold_tile continues the running sum over them in ascending order, with
 // the same random bits -- the result does not depend on the plan.
 #include "fp8t_device.h"
 #include "fp8train.h"
@@ -46,17 +57,17 @@ constexpr int kBK = 32;               // k per LDS slab (a multiple of 8)
 constexpr int kPitch = kBM + 4;       // floats per LDS row
 constexpr size_t kWsAlign = 256;
 
-struct SrArgs {
-    const uint8_t* A;
-    const uint8_t* B;
+struct TileArgs {
+    const void* A;
+    const void* B;
     uint16_t* C;
     uint16_t* ws;                     // chunk sums of the shared tiles
     int64_t lda, ldb, ldc;
     int M, N, K, CL;
-    uint32_t k0, k1;                  // Philox key
+    uint32_t k0, k1;                  // Philox key (stochastic rounding)
     uint32_t w3;                      // 2 * offset
     int c_vec;                        // C rows allow 8-byte stores of 4 codes
-    int a_vec, b_vec;                 // A / B rows allow 8-byte loads
+    int a_vec, b_vec;                 // A / B rows allow 8-element loads
 };
 
 // Uniform-derived addend: (2^14 - 1) - (u >> 2) for the 16-bit uniform in
@@ -71,37 +82,87 @@ __device__ __forceinline__ float sr16s(float x, uint32_t add) {
 }
 
 __device__ __forceinline__ u32x4 block_of(uint32_t i, uint32_t j, uint32_t q, uint32_t w3,
-                                          const SrArgs& g) {
+                                          const TileArgs& g) {
     const u32x4 c = {i, j, q, w3};
     return philox4x32_10(c, g.k0, g.k1);
 }
 
-// Stage a whole slab (64 rows x 32 k, all inside the matrix, 8-byte aligned
-// rows) with one 8-byte load per thread.  KC: k is contiguous in memory
+// FP16 code -> value * 2^S (exact).
+template <int S>
+__device__ __forceinline__ float fp16_to_f32_shift(uint32_t c) {
+    const uint32_t e = (c >> 9) & 63u, m = c & 511u;
+    uint32_t bits;
+    if (e == 63u)
+        bits = m ? kF32NaN : kF32Inf;
+    else if (e == 0u)
+        bits = __float_as_uint((float)m * __builtin_ldexpf(1.0f, S - 39));
+    else
+        bits = ((c & 0x7FFFu) << 14) + ((uint32_t)(96 + S) << 23);
+    return __uint_as_float(bits | ((c & 0x8000u) << 16));
+}
+
+// Operand element (code) -> float in the kernel's domain: FP8 A scaled by
+// 2^96, FP8 B plain; FP16 A and B scaled by 2^48 each.
+template <int FMT, bool IS_A>
+__device__ __forceinline__ float decode(uint32_t c) {
+    if (FMT == 8) return IS_A ? fp8_to_f32<96>(c) : fp8_to_f32<0>(c);
+    return fp16_to_f32_shift<48>(c);
+}
+
+template <int FMT> struct Elem;
+template <> struct Elem<8> { typedef uint8_t t; typedef uint2 v8; };
+template <> struct Elem<16> { typedef uint16_t t; typedef uint4 v8; };
+
+// Stage a whole slab (64 rows x 32 k, all inside the matrix, aligned rows)
+// with one 8-element load per thread.  KC: k is contiguous in memory
 // (element (r, k) at p[r * ld + k]); otherwise the row index is.
-template <bool KC, int SHIFT>
-__device__ __forceinline__ void stage_fast(const uint8_t* __restrict__ p, int64_t ld, int r0,
-                                           int k0, float (*X)[kPitch], int tid) {
+template <int FMT, bool IS_A, bool KC>
+__device__ __forceinline__ void stage_fast(const typename Elem<FMT>::t* __restrict__ p,
+                                           int64_t ld, int r0, int k0, float (*X)[kPitch],
+                                           int tid) {
+    typedef typename Elem<FMT>::v8 V;
+    uint32_t w[FMT / 4];
+    float f[8];
+    int r, kq, k, rq;
     if (KC) {
-        const int r = tid / (kBK / 8), kq = (tid % (kBK / 8)) * 8;
-        const uint2 v = *reinterpret_cast<const uint2*>(p + (int64_t)(r0 + r) * ld + k0 + kq);
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-            X[kq + e][r] = fp8_to_f32<SHIFT>(((e < 4 ? v.x : v.y) >> (8 * (e % 4))) & 0xFFu);
+        r = tid / (kBK / 8), kq = (tid % (kBK / 8)) * 8;
+        const V v = *reinterpret_cast<const V*>(p + (int64_t)(r0 + r) * ld + k0 + kq);
+        __builtin_memcpy(w, &v, sizeof(v));
     } else {
-        const int k = tid / (kBM / 8), rq = (tid % (kBM / 8)) * 8;
-        const uint2 v = *reinterpret_cast<const uint2*>(p + (int64_t)(k0 + k) * ld + r0 + rq);
-        float f[8];
+        k = tid / (kBM / 8), rq = (tid % (kBM / 8)) * 8;
+        const V v = *reinterpret_cast<const V*>(p + (int64_t)(k0 + k) * ld + r0 + rq);
+        __builtin_memcpy(w, &v, sizeof(v));
+    }
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-            f[e] = fp8_to_f32<SHIFT>(((e < 4 ? v.x : v.y) >> (8 * (e % 4))) & 0xFFu);
+    for (int e = 0; e < 8; ++e) {
+        const uint32_t c = FMT == 8 ? (w[e / 4] >> (8 * (e % 4))) & 0xFFu
+                                    : (w[e / 2] >> (16 * (e % 2))) & 0xFFFFu;
+        f[e] = decode<FMT, IS_A>(c);
+    }
+    if (KC) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) X[kq + e][r] = f[e];
+    } else {
         *reinterpret_cast<float4*>(&X[k][rq]) = make_float4(f[0], f[1], f[2], f[3]);
         *reinterpret_cast<float4*>(&X[k][rq + 4]) = make_float4(f[4], f[5], f[6], f[7]);
     }
 }
 
-template <bool TA, bool TB>
-__global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
+// FP16 product in the 2^96 domain rounded to FP16 (nearest even): raw-bit
+// rounding of the significand, or a multiple of 2^-39 below 2^-30.
+__device__ __forceinline__ float round_product16(float p) {
+    const float kMagic = 0x1.8p80f;            // 1.5 x 2^80: step 2^57 there
+    const float sub = (p + kMagic) - kMagic;
+    return __builtin_fabsf(p) < 0x1p66f ? sub : rn16s(p);
+}
+
+// FMT: operand format (8 = FP8 codes, 16 = FP16 codes); SR: stochastic
+// rounding of every addition (else nearest).
+template <bool TA, bool TB, int FMT, bool SR>
+__global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p) {
+    typedef typename Elem<FMT>::t E;
+    const E* __restrict__ A = static_cast<const E*>(g.A);
+    const E* __restrict__ B = static_cast<const E*>(g.B);
     __shared__ __attribute__((aligned(16))) float As[kBK][kPitch];
     __shared__ __attribute__((aligned(16))) float Bs[kBK][kPitch];
     const int tid = threadIdx.x;
@@ -136,7 +197,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
                     v.y = (uint32_t)f32s_to_fp16(P[r][2]) | ((uint32_t)f32s_to_fp16(P[r][3]) << 16);
                     *reinterpret_cast<uint2*>(dst + r * kBN) = v;
                 }
-            } else {
+            } else if (SR) {
                 // uniforms 4 (tx mod 2) + c of block (i, j / 8, chunk)
                 const bool odd = tx & 1;
 #pragma unroll
@@ -147,6 +208,11 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
                     for (int c = 0; c < kT; ++c)
                         S[r][c] = sr16s(S[r][c] + P[r][c], sr_addend(c < 2 ? w0 : w1, c % 2));
                 }
+            } else {
+#pragma unroll
+                for (int r = 0; r < kT; ++r)
+#pragma unroll
+                    for (int c = 0; c < kT; ++c) S[r][c] = rn16s(S[r][c] + P[r][c]);
             }
 #pragma unroll
             for (int r = 0; r < kT; ++r)
@@ -161,10 +227,10 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
             const int lo = sb > kbeg ? sb : kbeg;
             const int hi = sb + kBK < kend ? sb + kBK : kend;
             __syncthreads();               // the previous slab is consumed
-            // stage op(A)[m0.., lo..hi) and op(B)[lo..hi), n0..) as floats
-            // (A scaled by 2^96); rows, columns and k outside are zero
+            // stage op(A)[m0.., lo..hi) and op(B)[lo..hi), n0..) as floats;
+            // rows, columns and k outside are zero
             if (lo == sb && hi == sb + kBK && m0 + kBM <= g.M && g.a_vec) {
-                stage_fast<!TA, 96>(g.A, g.lda, m0, sb, As, tid);
+                stage_fast<FMT, true, !TA>(A, g.lda, m0, sb, As, tid);
             } else {
 #pragma unroll
                 for (int q = 0; q < kBM * kBK / kNT; ++q) {
@@ -174,12 +240,12 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
                     const int m = m0 + mm, k = sb + kk;
                     uint32_t code = 0;
                     if (m < g.M && k >= lo && k < hi)
-                        code = TA ? g.A[(int64_t)k * g.lda + m] : g.A[(int64_t)m * g.lda + k];
-                    As[kk][mm] = fp8_to_f32<96>(code);
+                        code = TA ? A[(int64_t)k * g.lda + m] : A[(int64_t)m * g.lda + k];
+                    As[kk][mm] = decode<FMT, true>(code);
                 }
             }
             if (lo == sb && hi == sb + kBK && n0 + kBN <= g.N && g.b_vec) {
-                stage_fast<TB, 0>(g.B, g.ldb, n0, sb, Bs, tid);
+                stage_fast<FMT, false, TB>(B, g.ldb, n0, sb, Bs, tid);
             } else {
 #pragma unroll
                 for (int q = 0; q < kBN * kBK / kNT; ++q) {
@@ -189,8 +255,8 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
                     const int n = n0 + nn, k = sb + kk;
                     uint32_t code = 0;
                     if (n < g.N && k >= lo && k < hi)
-                        code = TB ? g.B[(int64_t)n * g.ldb + k] : g.B[(int64_t)k * g.ldb + n];
-                    Bs[kk][nn] = fp8_to_f32<0>(code);
+                        code = TB ? B[(int64_t)n * g.ldb + k] : B[(int64_t)k * g.ldb + n];
+                    Bs[kk][nn] = decode<FMT, false>(code);
                 }
             }
             __syncthreads();
@@ -198,13 +264,15 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
             for (int gq = lo & ~1; gq < hi; gq += 2) {
                 // rows' blocks for k = gq, gq + 1 (complemented words)
                 uint32_t nw[kT][4];
+                if (SR) {
 #pragma unroll
-                for (int r = 0; r < kT; ++r) {
-                    const u32x4 b = block_of(gi + r, gj >> 2, (uint32_t)(gq >> 1), g.w3, g);
-                    nw[r][0] = ~b.x;
-                    nw[r][1] = ~b.y;
-                    nw[r][2] = ~b.z;
-                    nw[r][3] = ~b.w;
+                    for (int r = 0; r < kT; ++r) {
+                        const u32x4 b = block_of(gi + r, gj >> 2, (uint32_t)(gq >> 1), g.w3, g);
+                        nw[r][0] = ~b.x;
+                        nw[r][1] = ~b.y;
+                        nw[r][2] = ~b.z;
+                        nw[r][3] = ~b.w;
+                    }
                 }
 #pragma unroll
                 for (int s = 0; s < 2; ++s) {
@@ -217,16 +285,23 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
 #pragma unroll
                     for (int r = 0; r < kT; ++r)
 #pragma unroll
-                        for (int c = 0; c < kT; ++c)
-                            P[r][c] = sr16s(__builtin_fmaf(av[r], bv[c], P[r][c]),
-                                            sr_addend(nw[r][2 * s + c / 2], c % 2));
+                        for (int c = 0; c < kT; ++c) {
+                            float x;
+                            if (FMT == 8) {
+                                x = __builtin_fmaf(av[r], bv[c], P[r][c]);
+                            } else {
+                                x = P[r][c] + round_product16(av[r] * bv[c]);
+                            }
+                            P[r][c] = SR ? sr16s(x, sr_addend(nw[r][2 * s + c / 2], c % 2))
+                                         : rn16s(x);
+                        }
                     if (k + 1 == cend) chunk_end();
                 }
             }
         }
         if (to_ws) return;
         // the running sum: the result of a whole tile, or the start of a
-        // shared tile's chain (continued by chunk_fold_sr)
+        // shared tile's chain (continued by chunk_fold_tile)
 #pragma unroll
         for (int r = 0; r < kT; ++r) {
             const int m = m0 + ty * kT + r, n = n0 + tx * kT;
@@ -262,13 +337,15 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_sr_kernel(SrArgs g, Plan p) {
 }
 
 // Continue the running sums of the shared tiles (in C, from their first
-// pieces) over the chunk sums in the workspace, in ascending chunk order, with
-// the inter-chunk uniforms -- the additions a whole-tile pass makes.  A thread
-// takes 8 consecutive outputs of a row: one block of uniforms and one 16-byte
-// load of chunk sums per chunk.
+// pieces) over the chunk sums in the workspace, in ascending chunk order --
+// the additions a whole-tile pass makes, with the same rounding (and, for
+// SR, the same inter-chunk uniforms).  A thread takes 8 consecutive outputs
+// of a row: one 16-byte load of chunk sums (and one block of uniforms) per
+// chunk.
 constexpr int kFoldV = 8;
 
-__global__ __launch_bounds__(256) void chunk_fold_sr(SrArgs g, Plan p) {
+template <bool SR>
+__global__ __launch_bounds__(256) void chunk_fold_tile(TileArgs g, Plan p) {
     const int64_t per = (int64_t)kBM * kBN;
     const int64_t idx = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kFoldV;
     const int64_t lt = idx / per;
@@ -289,12 +366,19 @@ __global__ __launch_bounds__(256) void chunk_fold_sr(SrArgs g, Plan p) {
     for (int c = a; c < p.nch; ++c) {
         const uint4 q = src[(int64_t)c * (per / kFoldV)];
         const uint32_t cw[4] = {q.x, q.y, q.z, q.w};
-        const u32x4 b = block_of((uint32_t)m, (uint32_t)(n0 >> 3), (uint32_t)c, g.w3 + 1u, g);
-        const uint32_t nw[4] = {~b.x, ~b.y, ~b.z, ~b.w};
+        uint32_t nw[4] = {0u, 0u, 0u, 0u};
+        if (SR) {
+            const u32x4 b = block_of((uint32_t)m, (uint32_t)(n0 >> 3), (uint32_t)c, g.w3 + 1u, g);
+            nw[0] = ~b.x;
+            nw[1] = ~b.y;
+            nw[2] = ~b.z;
+            nw[3] = ~b.w;
+        }
 #pragma unroll
-        for (int v = 0; v < kFoldV; ++v)
-            S[v] = sr16s(S[v] + fp16_to_f32s((cw[v / 2] >> (16 * (v % 2))) & 0xFFFFu),
-                         sr_addend(nw[v / 2], v % 2));
+        for (int v = 0; v < kFoldV; ++v) {
+            const float x = S[v] + fp16_to_f32s((cw[v / 2] >> (16 * (v % 2))) & 0xFFFFu);
+            S[v] = SR ? sr16s(x, sr_addend(nw[v / 2], v % 2)) : rn16s(x);
+        }
     }
 #pragma unroll
     for (int v = 0; v < kFoldV; ++v)
@@ -307,14 +391,15 @@ __global__ void fill_zero16(uint16_t* __restrict__ C, int64_t ldc, int M, int N)
     C[(i / N) * ldc + i % N] = 0;
 }
 
-const void* sr_kernel(int ta, int tb) {
-    if (!ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_sr_kernel<false, false>);
-    if (!ta && tb) return reinterpret_cast<const void*>(&chunk_gemm_sr_kernel<false, true>);
-    if (ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_sr_kernel<true, false>);
-    return reinterpret_cast<const void*>(&chunk_gemm_sr_kernel<true, true>);
+template <int FMT, bool SR>
+const void* tile_kernel(int ta, int tb) {
+    if (!ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_tile_kernel<false, false, FMT, SR>);
+    if (!ta && tb) return reinterpret_cast<const void*>(&chunk_gemm_tile_kernel<false, true, FMT, SR>);
+    if (ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_tile_kernel<true, false, FMT, SR>);
+    return reinterpret_cast<const void*>(&chunk_gemm_tile_kernel<true, true, FMT, SR>);
 }
 
-struct SrPlan {
+struct TilePlan {
     Plan plan;
     size_t ws_bytes = 0;
     bool ok = false;
@@ -323,10 +408,10 @@ struct SrPlan {
 // One workgroup per resident slot; with a workspace allowed, tiles that do
 // not divide evenly over the slots have their chunks shared out (every
 // workgroup then ends with the same number of chunks).
-SrPlan plan_sr(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, bool allow_ws) {
-    SrPlan r;
+TilePlan plan_tile(const void* fn, int64_t M, int64_t N, int64_t K, int64_t CL, bool allow_ws) {
+    TilePlan r;
     const int cus = device_cus();
-    const int occ = kernel_occupancy(sr_kernel(ta, tb), kNT);
+    const int occ = kernel_occupancy(fn, kNT);
     if (cus <= 0 || occ <= 0) return r;
     int64_t gmax = (int64_t)cus * occ;
     const int force_g = env_int("FP8T_GEMM_WGS", 0);
@@ -357,45 +442,31 @@ SrPlan plan_sr(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, bool
     }
     p.xcd_remap = p.t_whole % 8 == 0 && p.G % 8 == 0;
     if (env_int("FP8T_GEMM_VERBOSE", 0))
-        fprintf(stderr, "[fp8t sr plan] occ %d G %d T %lld t_whole %lld L %lld ws %zu\n", occ,
+        fprintf(stderr, "[fp8t tile plan] occ %d G %d T %lld t_whole %lld L %lld ws %zu\n", occ,
                 p.G, (long long)T, (long long)p.t_whole, (long long)p.L, r.ws_bytes);
     r.plan = p;
     r.ok = true;
     return r;
 }
 
-bool sr_args_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, uint64_t offset) {
+bool tile_args_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL) {
     if (M < 0 || N < 0 || K < 0 || CL < 1) return false;
     if ((ta != 0 && ta != 1) || (tb != 0 && tb != 1)) return false;
     // 32-bit indices inside the kernel (k also runs one slab past K)
-    if (M > INT32_MAX || N > INT32_MAX || K > INT32_MAX - 2 * kBK) return false;
-    return offset < 0x80000000ull;
+    return M <= INT32_MAX && N <= INT32_MAX && K <= INT32_MAX - 2 * kBK;
 }
 
-}  // namespace
-}  // namespace fp8t
-
-using namespace fp8t;
-
-extern "C" size_t chunk_gemm_sr_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N,
-                                               int64_t K, int64_t CL) {
-    if (!sr_args_ok(trans_a, trans_b, M, N, K, CL, 0)) return 0;
-    if (M == 0 || N == 0 || K == 0) return 0;
-    const SrPlan sp = plan_sr(trans_a, trans_b, M, N, K, CL > K ? K : CL, true);
-    return sp.ok ? sp.ws_bytes : 0;
-}
-
-extern "C" int chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
-                             int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
-                             int64_t ldb, uint16_t* C, int64_t ldc, uint64_t seed,
-                             uint64_t offset, void* workspace, size_t workspace_bytes,
-                             hipStream_t stream) {
-    if (!sr_args_ok(trans_a, trans_b, M, N, K, CL, offset)) return FP8T_EINVAL;
+// Validation, K = 0, planning and launch shared by the two entry points.
+template <int FMT, bool SR>
+int tile_call(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, const void* A,
+              int64_t lda, const void* B, int64_t ldb, uint16_t* C, int64_t ldc, uint64_t seed,
+              uint64_t offset, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    if (!tile_args_ok(ta, tb, M, N, K, CL)) return FP8T_EINVAL;
     if (M == 0 || N == 0) return FP8T_OK;
     if (!C || ldc < N) return FP8T_EINVAL;
     if (K > 0) {
         if (!A || !B) return FP8T_EINVAL;
-        if (lda < (trans_a ? M : K) || ldb < (trans_b ? K : N)) return FP8T_EINVAL;
+        if (lda < (ta ? M : K) || ldb < (tb ? K : N)) return FP8T_EINVAL;
     }
     if (workspace_bytes > 0 && !workspace) return FP8T_EINVAL;
     if (K == 0) {
@@ -405,14 +476,15 @@ extern "C" int chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int
         return launch_status();
     }
     if (CL > K) CL = K;
-    const SrPlan sp = plan_sr(trans_a, trans_b, M, N, K, CL, workspace_bytes > 0);
-    if (!sp.ok) return FP8T_EHIP;
-    if (sp.ws_bytes > workspace_bytes) return FP8T_EWORKSPACE;
-    SrArgs g{};
+    const void* fn = tile_kernel<FMT, SR>(ta, tb);
+    const TilePlan tp = plan_tile(fn, M, N, K, CL, workspace_bytes > 0);
+    if (!tp.ok) return FP8T_EHIP;
+    if (tp.ws_bytes > workspace_bytes) return FP8T_EWORKSPACE;
+    TileArgs g{};
     g.A = A;
     g.B = B;
     g.C = C;
-    if (sp.plan.L > 0)
+    if (tp.plan.L > 0)
         g.ws = reinterpret_cast<uint16_t*>(((uintptr_t)workspace + kWsAlign - 1) &
                                            ~(uintptr_t)(kWsAlign - 1));
     g.lda = lda;
@@ -426,17 +498,58 @@ extern "C" int chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int
     g.k1 = (uint32_t)(seed >> 32);
     g.w3 = 2u * (uint32_t)offset;
     g.c_vec = aligned(C, 8) && ldc % 4 == 0;
-    g.a_vec = aligned(A, 8) && lda % 8 == 0;
-    g.b_vec = aligned(B, 8) && ldb % 8 == 0;
-    Plan plan = sp.plan;
+    const int eb = FMT / 8;                   // bytes per element
+    g.a_vec = aligned(A, 8 * eb) && lda % 8 == 0;
+    g.b_vec = aligned(B, 8 * eb) && ldb % 8 == 0;
+    Plan plan = tp.plan;
     void* args[] = {&g, &plan};
-    if (hipLaunchKernel(sr_kernel(trans_a, trans_b), dim3(plan.G), dim3(kNT), args, 0, stream) !=
-        hipSuccess)
+    if (hipLaunchKernel(fn, dim3(plan.G), dim3(kNT), args, 0, stream) != hipSuccess)
         return FP8T_EHIP;
     if (plan.L > 0) {
         const int64_t threads = (plan.L / plan.nch) * kBM * kBN / kFoldV;
-        hipLaunchKernelGGL(chunk_fold_sr, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
-                           stream, g, plan);
+        hipLaunchKernelGGL(chunk_fold_tile<SR>, dim3((unsigned)((threads + 255) / 256)),
+                           dim3(256), 0, stream, g, plan);
     }
     return launch_status();
+}
+
+template <int FMT, bool SR>
+size_t tile_workspace(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL) {
+    if (!tile_args_ok(ta, tb, M, N, K, CL)) return 0;
+    if (M == 0 || N == 0 || K == 0) return 0;
+    const TilePlan tp = plan_tile(tile_kernel<FMT, SR>(ta, tb), M, N, K, CL > K ? K : CL, true);
+    return tp.ok ? tp.ws_bytes : 0;
+}
+
+}  // namespace
+}  // namespace fp8t
+
+using namespace fp8t;
+
+extern "C" size_t chunk_gemm_sr_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N,
+                                               int64_t K, int64_t CL) {
+    return tile_workspace<8, true>(trans_a, trans_b, M, N, K, CL);
+}
+
+extern "C" int chunk_gemm_sr(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                             int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+                             int64_t ldb, uint16_t* C, int64_t ldc, uint64_t seed,
+                             uint64_t offset, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream) {
+    if (offset >= 0x80000000ull) return FP8T_EINVAL;
+    return tile_call<8, true>(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, seed,
+                              offset, workspace, workspace_bytes, stream);
+}
+
+extern "C" size_t chunk_gemm_p16_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N,
+                                                int64_t K, int64_t CL) {
+    return tile_workspace<16, false>(trans_a, trans_b, M, N, K, CL);
+}
+
+extern "C" int chunk_gemm_p16(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                              int64_t CL, const uint16_t* A, int64_t lda, const uint16_t* B,
+                              int64_t ldb, uint16_t* C, int64_t ldc, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+    return tile_call<16, false>(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, 0, 0,
+                                workspace, workspace_bytes, stream);
 }

@@ -35,6 +35,7 @@ def test_header_declares_the_boundary():
         "fp8_quantize", "fp16_quantize", "chunk_gemm", "chunk_gemm_workspace_size",
         "chunk_gemm_fp8", "chunk_gemm_fp8_workspace_size",
         "chunk_gemm_sr", "chunk_gemm_sr_workspace_size", "adam_update",
+        "chunk_gemm_p16", "chunk_gemm_p16_workspace_size",
         "sr_weight_update", "fp8t_status_string"])
 
 
@@ -140,6 +141,26 @@ def test_chunk_gemm_sr_rejects(lib):
     assert _gemm_sr(lib, ws=None, wsb=64) == E
     assert _gemm_sr(lib, M=0) == fp8t.OK
     assert fp8t.chunk_gemm_sr_workspace_size(0, 0, 4, 4, 4, 0) == 0
+
+
+def test_chunk_gemm_p16_rejects(lib):
+    E = fp8t.EINVAL
+    f = lib.chunk_gemm_p16
+
+    def call(**kw):
+        a = dict(ta=0, tb=0, M=4, N=4, K=4, CL=2, A=FAKE, lda=4, B=FAKE, ldb=4, C=FAKE, ldc=4,
+                 ws=None, wsb=0)
+        a.update(kw)
+        return f(a["ta"], a["tb"], a["M"], a["N"], a["K"], a["CL"], a["A"], a["lda"], a["B"],
+                 a["ldb"], a["C"], a["ldc"], a["ws"], a["wsb"], None)
+    assert call(CL=0) == E
+    assert call(tb=2) == E
+    assert call(lda=3) == E
+    assert call(ldc=3) == E
+    assert call(A=None) == E
+    assert call(ws=None, wsb=8) == E
+    assert call(N=0) == fp8t.OK
+    assert fp8t.chunk_gemm_p16_workspace_size(0, 0, 4, 4, 4, 0) == 0
 
 
 def test_workspace_size_without_a_device(lib):
