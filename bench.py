@@ -158,7 +158,10 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
       (momentum 0.9, weight decay 1e-4, FP8 copy), against HBM;
     * chunk_gemm_sr (stochastic rounding after every FP16 addition) on the
       forward and weight-gradient shapes, against its ALU ceiling;
-    * adam_update at 25.6 M parameters, against HBM."""
+    * adam_update at 25.6 M parameters, against HBM;
+    * one whole training step of the speech DNN (440 -> 1024 x 5 -> 6000,
+      batch 256; FP8 hidden layers, FP16 last layer, loss scale 1000, SR
+      update) in exact and fast mode."""
     out = {}
     sr = {}
     for name, (ta, tb, m_, n_, k_, A, B) in (("fwd", (0, 0, M, N, K, X8, W8)),
@@ -209,7 +212,38 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
                                                  1e-8, 1e-4, 10, 7, 0), 20)
     out["adam_update_25_6M"] = {"us": t * 1e3, "gb_s": 15 * n / (t * 1e-3) / 1e9,
                                 "frac_of_hbm": 15 * n / (t * 1e-3) / HBM_BYTES_S}
+    del w16, g16, v16, w8, m16, s16
+    out["speech_dnn_step"] = mlp_measurement(torch, fp8t)
     return out
+
+
+def mlp_measurement(torch, fp8t):
+    import workloads
+    from paper_1812_08011_amd.mlp import SPEECH_DNN, Fp8Mlp
+    d = workloads.speech_mlp()
+    res = {}
+    for mode, tag in ((fp8t.EXACT, "exact"), (fp8t.FAST, "fast")):
+        net = Fp8Mlp(SPEECH_DNN, 256, mode=mode)
+        W16 = []
+        for w in d["W"]:
+            t16 = torch.empty(w.shape, dtype=torch.uint16, device="cuda")
+            fp8t.fp16_quantize(torch.from_numpy(w).cuda(), t16)
+            W16.append(t16.cpu().view(torch.int16).numpy().view(np.uint16))
+        net.set_weights(W16)
+        X8 = torch.empty(d["X"].shape, dtype=torch.uint8, device="cuda")
+        fp8t.fp8_quantize(torch.from_numpy(d["X"]).cuda(), X8)
+        T16 = torch.empty(d["T"].shape, dtype=torch.uint16, device="cuda")
+        fp8t.fp16_quantize(torch.from_numpy(d["T"]).cuda(), T16)
+        step = [0]
+
+        def f():
+            step[0] += 1
+            net.step(X8, T16, d["lr"], d["momentum"], d["weight_decay"], d["loss_scale"],
+                     d["seed"], step[0])
+        ms = time_ms(torch, f, 10)
+        res[tag] = {"ms": ms, "tmac_s": net.macs() / (ms * 1e-3) / 1e12}
+        del net
+    return res
 
 
 def main():

@@ -288,6 +288,31 @@ int adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,
                 float eps, float weight_decay, uint64_t t, uint64_t seed,
                 uint64_t offset, hipStream_t stream);
 
+/*
+ * Element-wise steps of a training step around the GEMMs (Sec. 2.1: the
+ * activations and errors enter the GEMMs in FP8; Sec. 3: loss scaling and
+ * an FP16 last layer).  n >= 0 contiguous elements; n == 0 is a no-op.
+ * Errors: FP8T_EINVAL (n < 0, a NULL pointer with n > 0, unknown format);
+ * FP8T_EHIP.
+ *
+ * relu_codes: y[i] = ReLU(x[i]) on codes of `format` 8 (FP8, uint8_t) or 16
+ *   (FP16, uint16_t): negative values (-0 and -Inf included) become +0, NaN
+ *   becomes the canonical NaN code, other codes are copied.  ReLU commutes
+ *   with rounding to FP8, so ReLU(Q8(z)) == Q8(ReLU(z)).  y may equal x.
+ * relu_backward_fp8: e[i] = Q8(RN32(value(d[i]) * scale)) where
+ *   value(z[i]) > 0, else +0 -- the ReLU derivative applied to an FP16 error
+ *   d (z is the layer's FP16 pre-activation) and the result rounded to FP8
+ *   for the next Backward/Gradient GEMMs.
+ * mse_grad_fp16: e[i] = RN16(RN32(RN32(value(y[i]) - value(t[i])) * scale)),
+ *   the loss-scaled gradient of a squared-error loss (scale = loss scale /
+ *   batch) in FP16.
+ */
+int relu_codes(const void* x, int format, void* y, int64_t n, hipStream_t stream);
+int relu_backward_fp8(const uint16_t* d, const uint16_t* z, uint8_t* e, int64_t n,
+                      float scale, hipStream_t stream);
+int mse_grad_fp16(const uint16_t* y, const uint16_t* t, uint16_t* e, int64_t n,
+                  float scale, hipStream_t stream);
+
 /* A static, human-readable description of a status code. */
 const char* fp8t_status_string(int status);
 

@@ -60,6 +60,12 @@ def lib():
                                      vp, sz, vp]
         L.chunk_gemm_p16_workspace_size.restype = sz
         L.chunk_gemm_p16_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64]
+        L.relu_codes.restype = i32
+        L.relu_codes.argtypes = [vp, i32, vp, i64, vp]
+        L.relu_backward_fp8.restype = i32
+        L.relu_backward_fp8.argtypes = [vp, vp, vp, i64, f32, vp]
+        L.mse_grad_fp16.restype = i32
+        L.mse_grad_fp16.argtypes = [vp, vp, vp, i64, f32, vp]
         L.adam_update.restype = i32
         L.adam_update.argtypes = [vp, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, u64, u64,
                                   u64, vp]
@@ -210,3 +216,21 @@ def chunk_gemm_p16(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, worksp
                                 _ptr(A), int(lda), _ptr(B), int(ldb), _ptr(C), int(ldc),
                                 _ptr(workspace), int(workspace_bytes), _stream(stream)))
     return C
+
+
+def relu_codes(x, fmt, y, n, stream=None):
+    """ReLU on FP8 (fmt 8) or FP16 (fmt 16) codes; y may be x."""
+    _check("relu_codes", lib().relu_codes(_ptr(x), int(fmt), _ptr(y), int(n), _stream(stream)))
+    return y
+
+
+def relu_backward_fp8(d, z, e, n, scale=1.0, stream=None):
+    _check("relu_backward_fp8", lib().relu_backward_fp8(_ptr(d), _ptr(z), _ptr(e), int(n),
+                                                        float(scale), _stream(stream)))
+    return e
+
+
+def mse_grad_fp16(y, t, e, n, scale, stream=None):
+    _check("mse_grad_fp16", lib().mse_grad_fp16(_ptr(y), _ptr(t), _ptr(e), int(n), float(scale),
+                                                _stream(stream)))
+    return e

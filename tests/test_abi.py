@@ -36,6 +36,7 @@ def test_header_declares_the_boundary():
         "chunk_gemm_fp8", "chunk_gemm_fp8_workspace_size",
         "chunk_gemm_sr", "chunk_gemm_sr_workspace_size", "adam_update",
         "chunk_gemm_p16", "chunk_gemm_p16_workspace_size",
+        "relu_codes", "relu_backward_fp8", "mse_grad_fp16",
         "sr_weight_update", "fp8t_status_string"])
 
 
@@ -161,6 +162,18 @@ def test_chunk_gemm_p16_rejects(lib):
     assert call(ws=None, wsb=8) == E
     assert call(N=0) == fp8t.OK
     assert fp8t.chunk_gemm_p16_workspace_size(0, 0, 4, 4, 4, 0) == 0
+
+
+def test_elementwise_rejects(lib):
+    E = fp8t.EINVAL
+    assert lib.relu_codes(FAKE, 7, FAKE, 4, None) == E
+    assert lib.relu_codes(FAKE, 8, FAKE, -1, None) == E
+    assert lib.relu_codes(None, 16, FAKE, 4, None) == E
+    assert lib.relu_codes(None, 16, None, 0, None) == fp8t.OK
+    assert lib.relu_backward_fp8(FAKE, None, FAKE, 4, 1.0, None) == E
+    assert lib.relu_backward_fp8(FAKE, FAKE, FAKE, -2, 1.0, None) == E
+    assert lib.mse_grad_fp16(FAKE, FAKE, None, 4, 1.0, None) == E
+    assert lib.mse_grad_fp16(None, None, None, 0, 1.0, None) == fp8t.OK
 
 
 def test_workspace_size_without_a_device(lib):
