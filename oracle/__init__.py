@@ -84,6 +84,8 @@ def lib():
         L.cpu_chunk_gemm_p16_points.restype = ctypes.c_int
         L.cpu_chunk_gemm_p16_points.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64,
                                                 i64, vp, i64, vp, i64, vp, vp, i64, vp]
+        L.cpu_col2im.restype = ctypes.c_int
+        L.cpu_col2im.argtypes = [vp, i64, i64, i64, i64, i64, i64, i64, i64, vp]
         L.cpu_adam_update.restype = ctypes.c_int
         L.cpu_adam_update.argtypes = [vp, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, u64,
                                       u64, u64]

@@ -443,3 +443,40 @@ int cpu_adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,
     }
     return ORC_OK;
 }
+
+/* ---- col2im: the adjoint of the convolution lowering ----------------------
+ * Sec. 2.2 computes a convolution by lowering its input and a GEMM; the
+ * Backward GEMM then gives the error of the lowered matrix, and col2im adds
+ * each input position's entries back together.  For the NHWC input
+ * X[n, ih, iw, c] the lowered matrix has rows (n, oh, ow) and columns
+ * (kh, kw, c), entry X[n, oh*stride - pad + kh, ow*stride - pad + kw, c].
+ * Read here: dX[n, ih, iw, c] = the P16 sum, starting at +0, in ascending
+ * (kh, kw) order with rounding to nearest after every addition, of the
+ * entries that map to (n, ih, iw, c). */
+int cpu_col2im(const uint16_t* cols, int64_t N, int64_t H, int64_t W, int64_t C,
+               int64_t KH, int64_t KW, int64_t pad, int64_t stride, uint16_t* dX) {
+    if (N < 0 || H < 1 || W < 1 || C < 1 || KH < 1 || KW < 1 || pad < 0 || stride < 1)
+        return ORC_EINVAL;
+    if (H + 2 * pad < KH || W + 2 * pad < KW) return ORC_EINVAL;
+    const int64_t OH = (H + 2 * pad - KH) / stride + 1, OW = (W + 2 * pad - KW) / stride + 1;
+    const int64_t K = KH * KW * C;
+    if (N * H * W * C > 0 && (!cols || !dX)) return ORC_EINVAL;
+    #pragma omp parallel for schedule(static)
+    for (int64_t n = 0; n < N; n++)
+        for (int64_t ih = 0; ih < H; ih++)
+            for (int64_t iw = 0; iw < W; iw++)
+                for (int64_t c = 0; c < C; c++) {
+                    uint16_t S = 0;
+                    for (int64_t kh = 0; kh < KH; kh++)
+                        for (int64_t kw = 0; kw < KW; kw++) {
+                            const int64_t yh = ih + pad - kh, yw = iw + pad - kw;
+                            if (yh < 0 || yw < 0 || yh % stride || yw % stride) continue;
+                            const int64_t oh = yh / stride, ow = yw / stride;
+                            if (oh >= OH || ow >= OW) continue;
+                            S = orc_add16(S, cols[((n * OH + oh) * OW + ow) * K +
+                                                  (kh * KW + kw) * C + c]);
+                        }
+                    dX[((n * H + ih) * W + iw) * C + c] = S;
+                }
+    return ORC_OK;
+}

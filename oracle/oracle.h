@@ -102,6 +102,11 @@ int cpu_adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,
                     uint64_t offset);
 float orc_adam_step_size(float lr, float beta1, float beta2, uint64_t t);
 
+/* col2im of P16 codes (ops.c): the adjoint of the lowering of an NHWC
+ * convolution input, summed in P16 in ascending (kh, kw) order. */
+int cpu_col2im(const uint16_t* cols, int64_t N, int64_t H, int64_t W, int64_t C,
+               int64_t KH, int64_t KW, int64_t pad, int64_t stride, uint16_t* dX);
+
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int orc_num_threads(void);
 
