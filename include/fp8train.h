@@ -313,6 +313,58 @@ int relu_backward_fp8(const uint16_t* d, const uint16_t* z, uint8_t* e, int64_t 
 int mse_grad_fp16(const uint16_t* y, const uint16_t* t, uint16_t* e, int64_t n,
                   float scale, hipStream_t stream);
 
+/*
+ * Convolutions through an implicit lowering (Sec. 2.2: the convolution is
+ * computed by lowering its input, then a GEMM).  The input X is NHWC FP8
+ * (N x H x W x C, contiguous); output size OH = (H + 2 pad - KH) / stride + 1,
+ * OW likewise.  The lowered matrix Xcol has M = N OH OW rows (n, oh, ow) and
+ * K = KH KW C columns (kh, kw, c):
+ *   Xcol[(n, oh, ow), (kh, kw, c)] = X[n, oh*stride - pad + kh,
+ *                                      ow*stride - pad + kw, c]  (0 outside)
+ * and is never written out: the GEMM kernels read X directly.
+ *
+ * conv2d_fwd_fp8:   Y = chunk_gemm(Xcol, Wt), exact mode, bit for bit the
+ *   same as chunk_gemm on the explicit Xcol.  Wt: FP8 (K x Cout, row-major,
+ *   rows in (kh, kw, c) order); Y: FP16 codes, M x Cout, ldy >= Cout.
+ * conv2d_wgrad_fp8: dW = chunk_gemm(Xcol^T, dY), exact mode (as chunk_gemm
+ *   with trans_a = 1 on the explicit Xcol).  dY: FP8 (M x Cout); dW: FP16
+ *   codes, K x Cout, lddw >= Cout.
+ * The Backward GEMM needs no lowering (dXcol = chunk_gemm(dY, Wt^T),
+ * trans_b = 1); col2im_fp16 folds dXcol back onto the input.
+ * workspace: as chunk_gemm, sized by conv2d_workspace_size(wgrad, ...) (0 for
+ * invalid arguments).  C % 4 == 0 with a 4-byte aligned X reads 4 channels at
+ * a time; other channel counts are read byte by byte.
+ * Errors: FP8T_EINVAL (N < 0, H, W, C, KH, KW, stride < 1, pad < 0, a kernel
+ * larger than the padded input, Cout < 0, CL < 1, a NULL pointer for
+ * non-empty data, ldy / lddw < Cout, sizes beyond 32-bit indexing);
+ * FP8T_EWORKSPACE; FP8T_EHIP.
+ */
+int conv2d_fwd_fp8(const uint8_t* X, int64_t N, int64_t H, int64_t W, int64_t C,
+                   int64_t KH, int64_t KW, int64_t pad, int64_t stride,
+                   const uint8_t* Wt, int64_t Cout, int64_t CL, uint16_t* Y,
+                   int64_t ldy, void* workspace, size_t workspace_bytes,
+                   hipStream_t stream);
+int conv2d_wgrad_fp8(const uint8_t* X, int64_t N, int64_t H, int64_t W, int64_t C,
+                     int64_t KH, int64_t KW, int64_t pad, int64_t stride,
+                     const uint8_t* dY, int64_t Cout, int64_t CL, uint16_t* dW,
+                     int64_t lddw, void* workspace, size_t workspace_bytes,
+                     hipStream_t stream);
+size_t conv2d_workspace_size(int wgrad, int64_t N, int64_t H, int64_t W, int64_t C,
+                             int64_t KH, int64_t KW, int64_t pad, int64_t stride,
+                             int64_t Cout, int64_t CL);
+
+/*
+ * col2im_fp16 -- the adjoint of the lowering above for FP16 codes: for every
+ * input position, dX[n, ih, iw, c] = the FP16 sum, starting at +0, in
+ * ascending (kh, kw) order with rounding to nearest (ties to even) after
+ * every addition, of the entries cols[(n, oh, ow), (kh, kw, c)] that the
+ * lowering takes from (n, ih, iw, c).  cols: M x K FP16 codes (contiguous);
+ * dX: N x H x W x C FP16 codes.  Errors: as the convolutions; FP8T_EHIP.
+ */
+int col2im_fp16(const uint16_t* cols, int64_t N, int64_t H, int64_t W, int64_t C,
+                int64_t KH, int64_t KW, int64_t pad, int64_t stride, uint16_t* dX,
+                hipStream_t stream);
+
 /* A static, human-readable description of a status code. */
 const char* fp8t_status_string(int status);
 

@@ -66,6 +66,16 @@ def lib():
         L.relu_backward_fp8.argtypes = [vp, vp, vp, i64, f32, vp]
         L.mse_grad_fp16.restype = i32
         L.mse_grad_fp16.argtypes = [vp, vp, vp, i64, f32, vp]
+        L.conv2d_fwd_fp8.restype = i32
+        L.conv2d_fwd_fp8.argtypes = [vp, i64, i64, i64, i64, i64, i64, i64, i64, vp, i64, i64,
+                                     vp, i64, vp, sz, vp]
+        L.conv2d_wgrad_fp8.restype = i32
+        L.conv2d_wgrad_fp8.argtypes = list(L.conv2d_fwd_fp8.argtypes)
+        L.conv2d_workspace_size.restype = sz
+        L.conv2d_workspace_size.argtypes = [i32, i64, i64, i64, i64, i64, i64, i64, i64, i64,
+                                            i64]
+        L.col2im_fp16.restype = i32
+        L.col2im_fp16.argtypes = [vp, i64, i64, i64, i64, i64, i64, i64, i64, vp, vp]
         L.adam_update.restype = i32
         L.adam_update.argtypes = [vp, vp, vp, vp, vp, i64, f32, f32, f32, f32, f32, u64, u64,
                                   u64, vp]
@@ -234,3 +244,34 @@ def mse_grad_fp16(y, t, e, n, scale, stream=None):
     _check("mse_grad_fp16", lib().mse_grad_fp16(_ptr(y), _ptr(t), _ptr(e), int(n), float(scale),
                                                 _stream(stream)))
     return e
+
+
+def conv2d_workspace_size(wgrad, N, H, W, C, KH, KW, pad, stride, Cout, CL):
+    return int(lib().conv2d_workspace_size(int(wgrad), int(N), int(H), int(W), int(C), int(KH),
+                                           int(KW), int(pad), int(stride), int(Cout), int(CL)))
+
+
+def conv2d_fwd_fp8(X, N, H, W, C, KH, KW, pad, stride, Wt, Cout, CL, Y, ldy, workspace=None,
+                   workspace_bytes=0, stream=None):
+    _check("conv2d_fwd_fp8",
+           lib().conv2d_fwd_fp8(_ptr(X), int(N), int(H), int(W), int(C), int(KH), int(KW),
+                                int(pad), int(stride), _ptr(Wt), int(Cout), int(CL), _ptr(Y),
+                                int(ldy), _ptr(workspace), int(workspace_bytes), _stream(stream)))
+    return Y
+
+
+def conv2d_wgrad_fp8(X, N, H, W, C, KH, KW, pad, stride, dY, Cout, CL, dW, lddw, workspace=None,
+                     workspace_bytes=0, stream=None):
+    _check("conv2d_wgrad_fp8",
+           lib().conv2d_wgrad_fp8(_ptr(X), int(N), int(H), int(W), int(C), int(KH), int(KW),
+                                  int(pad), int(stride), _ptr(dY), int(Cout), int(CL), _ptr(dW),
+                                  int(lddw), _ptr(workspace), int(workspace_bytes),
+                                  _stream(stream)))
+    return dW
+
+
+def col2im_fp16(cols, N, H, W, C, KH, KW, pad, stride, dX, stream=None):
+    _check("col2im_fp16",
+           lib().col2im_fp16(_ptr(cols), int(N), int(H), int(W), int(C), int(KH), int(KW),
+                             int(pad), int(stride), _ptr(dX), _stream(stream)))
+    return dX

@@ -153,7 +153,7 @@ constexpr size_t kWsAlign = 256;
 // The best kernel configuration and work decomposition for these sizes; with
 // allow_ws false only plans that need no workspace are considered.
 Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL,
-                 bool allow_ws) {
+                 bool allow_ws, bool conv = false) {
     Choice best;
     const int cus = device_cus();
     if (cus <= 0) return best;
@@ -185,7 +185,7 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 t_tile = mfma_cost_per_tile(cfg);
             } else {
                 const ValuShape sh = valu_shape(cfg);
-                fn = valu_kernel(cfg, ta, tb, fast);
+                fn = conv ? valu_conv_kernel(cfg, ta) : valu_kernel(cfg, ta, tb, fast);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
                 t_out = (double)CL * valu_ops_per_mac(cfg) / (kLanesPerCU * kClockHz);
             }
@@ -389,4 +389,128 @@ extern "C" int chunk_gemm_fp8(int trans_a, int trans_b, int64_t M, int64_t N, in
                               size_t workspace_bytes, hipStream_t stream) {
     return gemm_call(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, C8, ldc8, scale,
                      mode, workspace, workspace_bytes, stream, true);
+}
+
+// ---------------------------------------------------------------------------
+// convolutions lowered implicitly (Sec. 2.2)
+// ---------------------------------------------------------------------------
+
+namespace {
+
+struct ConvShape {
+    int64_t M, K, OH, OW;   // M = N OH OW output pixels, K = KH KW C
+    bool ok;
+};
+
+ConvShape conv_shape(int64_t N, int64_t H, int64_t W, int64_t C, int64_t KH, int64_t KW,
+                     int64_t pad, int64_t stride) {
+    ConvShape r{0, 0, 0, 0, false};
+    if (N < 0 || H < 1 || W < 1 || C < 1 || KH < 1 || KW < 1 || pad < 0 || stride < 1)
+        return r;
+    r.OH = (H + 2 * pad - KH) / stride + 1;
+    r.OW = (W + 2 * pad - KW) / stride + 1;
+    if (H + 2 * pad < KH || W + 2 * pad < KW) return r;
+    r.M = N * r.OH * r.OW;
+    r.K = KH * KW * C;
+    // every index of X, Xcol and the GEMM in 32 bits
+    if (r.M > INT32_MAX || r.K > INT32_MAX || N * H * W * C > ((int64_t)1 << 40)) return r;
+    r.ok = true;
+    return r;
+}
+
+// The exact-mode GEMM with A = Xcol (wgrad: Xcol^T) read from the NHWC input.
+int conv_gemm_call(bool wgrad, const uint8_t* X, int64_t N, int64_t H, int64_t W, int64_t C,
+                   int64_t KH, int64_t KW, int64_t pad, int64_t stride, const uint8_t* B,
+                   int64_t Cout, int64_t CL, uint16_t* Out, int64_t ldo, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream, bool query, size_t* need) {
+    const ConvShape cs = conv_shape(N, H, W, C, KH, KW, pad, stride);
+    if (!cs.ok || Cout < 0 || CL < 1) return FP8T_EINVAL;
+    // GEMM dimensions: fwd  Y (M x Cout) = Xcol (M x K) W (K x Cout);
+    //                  wgrad dW (K x Cout) = Xcol^T (K x M) dY (M x Cout)
+    const int64_t gM = wgrad ? cs.K : cs.M, gN = Cout, gK = wgrad ? cs.M : cs.K;
+    const int ta = wgrad ? 1 : 0;
+    if (query) {
+        *need = 0;
+        if (gM == 0 || gN == 0 || gK == 0) return FP8T_OK;
+        const int64_t cl = CL > gK ? gK : CL;
+        *need = plan_workspace(plan_gemm(VALU_EXACT, ta, 0, gM, gN, gK, cl, true, true), false);
+        return FP8T_OK;
+    }
+    if (gM == 0 || gN == 0) return FP8T_OK;
+    if (!Out || ldo < gN) return FP8T_EINVAL;
+    if (gK > 0 && (!X || !B)) return FP8T_EINVAL;
+    if (workspace_bytes > 0 && !workspace) return FP8T_EINVAL;
+    if (gK == 0) {
+        const int64_t total = gM * gN;
+        hipLaunchKernelGGL(fill_empty, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                           stream, Out, ldo, (uint8_t*)nullptr, (int64_t)0, 1.0f, (int)gM,
+                           (int)gN);
+        return launch_status();
+    }
+    if (CL > gK) CL = gK;
+    const Choice ch = plan_gemm(VALU_EXACT, ta, 0, gM, gN, gK, CL, workspace_bytes > 0, true);
+    if (ch.cfg < 0) return FP8T_EHIP;
+    if (plan_workspace(ch, false) > workspace_bytes) return FP8T_EWORKSPACE;
+    GemmArgs g{};
+    g.A = X;
+    g.B = B;
+    g.C = Out;
+    if (ch.plan.L > 0) {
+        const uintptr_t base = ((uintptr_t)workspace + kWsAlign - 1) & ~(uintptr_t)(kWsAlign - 1);
+        g.ws = reinterpret_cast<uint16_t*>(base);
+    }
+    g.lda = wgrad ? cs.M : cs.K;          // not used: A is read through g.conv
+    g.ldb = Cout;
+    g.ldc = ldo;
+    g.M = (int)gM;
+    g.N = (int)gN;
+    g.K = (int)gK;
+    g.CL = (int)CL;
+    g.a_vec = 0;
+    g.b_vec = aligned(B, 4) && Cout % 4 == 0 && Cout < (1 << 24);
+    g.c_vec = aligned(Out, 4) && ldo % 2 == 0;
+    g.c_vec16 = aligned(Out, 16) && ldo % 8 == 0;
+    g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
+    g.conv.H = (int)H;
+    g.conv.W = (int)W;
+    g.conv.C = (int)C;
+    g.conv.KW = (int)KW;
+    g.conv.KWC = (int)(KW * C);
+    g.conv.OW = (int)cs.OW;
+    g.conv.OHW = (int)(cs.OH * cs.OW);
+    g.conv.pad = (int)pad;
+    g.conv.stride = (int)stride;
+    g.conv.vec = C % 4 == 0 && aligned(X, 4);
+    return launch_plan(ch, g, stream);
+}
+
+}  // namespace
+
+extern "C" int conv2d_fwd_fp8(const uint8_t* X, int64_t N, int64_t H, int64_t W, int64_t C,
+                              int64_t KH, int64_t KW, int64_t pad, int64_t stride,
+                              const uint8_t* Wt, int64_t Cout, int64_t CL, uint16_t* Y,
+                              int64_t ldy, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+    return conv_gemm_call(false, X, N, H, W, C, KH, KW, pad, stride, Wt, Cout, CL, Y, ldy,
+                          workspace, workspace_bytes, stream, false, nullptr);
+}
+
+extern "C" int conv2d_wgrad_fp8(const uint8_t* X, int64_t N, int64_t H, int64_t W, int64_t C,
+                                int64_t KH, int64_t KW, int64_t pad, int64_t stride,
+                                const uint8_t* dY, int64_t Cout, int64_t CL, uint16_t* dW,
+                                int64_t lddw, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream) {
+    return conv_gemm_call(true, X, N, H, W, C, KH, KW, pad, stride, dY, Cout, CL, dW, lddw,
+                          workspace, workspace_bytes, stream, false, nullptr);
+}
+
+extern "C" size_t conv2d_workspace_size(int wgrad, int64_t N, int64_t H, int64_t W, int64_t C,
+                                        int64_t KH, int64_t KW, int64_t pad, int64_t stride,
+                                        int64_t Cout, int64_t CL) {
+    size_t need = 0;
+    if (wgrad != 0 && wgrad != 1) return 0;
+    if (conv_gemm_call(wgrad != 0, nullptr, N, H, W, C, KH, KW, pad, stride, nullptr, Cout, CL,
+                       nullptr, 0, nullptr, 0, nullptr, true, &need) != FP8T_OK)
+        return 0;
+    return need;
 }

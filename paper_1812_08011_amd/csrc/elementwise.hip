@@ -58,6 +58,47 @@ __global__ __launch_bounds__(kThreads) void mse_grad_kernel(const uint16_t* __re
     }
 }
 
+// col2im: dX[n, ih, iw, c] = the FP16 sum, in ascending (kh, kw) order and
+// rounded to nearest after every addition, of the lowered-matrix entries
+// cols[(n, oh, ow), (kh, kw, c)] of the output positions whose window covers
+// (ih, iw).  One thread per element of dX, channels fastest (coalesced).
+struct Col2imGeom {
+    int64_t total;                     // N H W C
+    int H, W, C, KH, KW, OH, OW, pad, stride;
+    int64_t K;                         // KH KW C
+};
+
+__global__ __launch_bounds__(kThreads) void col2im_kernel(const uint16_t* __restrict__ cols,
+                                                          uint16_t* __restrict__ dx,
+                                                          Col2imGeom q) {
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < q.total; i += stride) {
+        const int c = (int)(i % q.C);
+        const int64_t pix = i / q.C;
+        const int iw = (int)(pix % q.W);
+        const int64_t t = pix / q.W;
+        const int ih = (int)(t % q.H);
+        const int64_t n = t / q.H;
+        float S = 0.0f;
+        for (int kh = 0; kh < q.KH; ++kh) {
+            const int yh = ih + q.pad - kh;
+            if (yh < 0 || yh % q.stride) continue;
+            const int oh = yh / q.stride;
+            if (oh >= q.OH) continue;
+            for (int kw = 0; kw < q.KW; ++kw) {
+                const int yw = iw + q.pad - kw;
+                if (yw < 0 || yw % q.stride) continue;
+                const int ow = yw / q.stride;
+                if (ow >= q.OW) continue;
+                const int64_t row = (n * q.OH + oh) * q.OW + ow;
+                const uint16_t v = cols[row * q.K + ((int64_t)kh * q.KW + kw) * q.C + c];
+                S = rn16s(S + fp16_to_f32s(v));
+            }
+        }
+        dx[i] = f32s_to_fp16(S);
+    }
+}
+
 unsigned grid_for(int64_t n) {
     int64_t g = (n + kThreads - 1) / kThreads;
     if (g > 256 * 64) g = 256 * 64;
@@ -99,5 +140,32 @@ extern "C" int mse_grad_fp16(const uint16_t* y, const uint16_t* t, uint16_t* e, 
     if (!y || !t || !e) return FP8T_EINVAL;
     hipLaunchKernelGGL(mse_grad_kernel, dim3(grid_for(n)), dim3(kThreads), 0, stream, y, t, e, n,
                        scale);
+    return launch_status();
+}
+
+extern "C" int col2im_fp16(const uint16_t* cols, int64_t N, int64_t H, int64_t W, int64_t C,
+                           int64_t KH, int64_t KW, int64_t pad, int64_t stride, uint16_t* dX,
+                           hipStream_t stream) {
+    if (N < 0 || H < 1 || W < 1 || C < 1 || KH < 1 || KW < 1 || pad < 0 || stride < 1)
+        return FP8T_EINVAL;
+    if (H + 2 * pad < KH || W + 2 * pad < KW) return FP8T_EINVAL;
+    if (H > INT32_MAX || W > INT32_MAX || C > INT32_MAX || KH * KW * C > INT32_MAX)
+        return FP8T_EINVAL;
+    Col2imGeom q;
+    q.total = N * H * W * C;
+    if (q.total == 0) return FP8T_OK;
+    if (!cols || !dX) return FP8T_EINVAL;
+    q.H = (int)H;
+    q.W = (int)W;
+    q.C = (int)C;
+    q.KH = (int)KH;
+    q.KW = (int)KW;
+    q.pad = (int)pad;
+    q.stride = (int)stride;
+    q.OH = (int)((H + 2 * pad - KH) / stride + 1);
+    q.OW = (int)((W + 2 * pad - KW) / stride + 1);
+    q.K = KH * KW * C;
+    hipLaunchKernelGGL(col2im_kernel, dim3(grid_for(q.total)), dim3(kThreads), 0, stream, cols,
+                       dX, q);
     return launch_status();
 }

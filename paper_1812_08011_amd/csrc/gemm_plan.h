@@ -24,6 +24,20 @@
 
 namespace fp8t {
 
+// Implicit lowering of a convolution (Sec. 2.2: a convolution is computed by
+// lowering its input and then a GEMM): the lowered matrix Xcol, M = N * OH *
+// OW rows (output pixels, row-major n, oh, ow) by KH * KW * C columns (order
+// kh, kw, c), is read straight from the NHWC input X:
+//   Xcol(p, (kh, kw, c)) = X[n, oh * stride - pad + kh, ow * stride - pad + kw, c]
+// (0 outside the image).
+struct ConvGeom {
+    int H, W, C;        // input height, width, channels
+    int KW, KWC;        // kernel width, KW * C
+    int OW, OHW;        // output width, OH * OW
+    int pad, stride;
+    int vec;            // C % 4 == 0 and X 4-byte aligned: 4 channels per load
+};
+
 struct GemmArgs {
     const uint8_t* A;
     const uint8_t* B;
@@ -41,6 +55,7 @@ struct GemmArgs {
     int c_vec16;        // C, ldc allow 16-byte stores (8 codes)
     int c8_vec8;        // C8, ldc8 allow 8-byte stores
     int guarded;        // exact mode: try the guarded path first
+    ConvGeom conv;      // A is the implicit lowering of an NHWC input (conv kernels)
 };
 
 struct Plan {

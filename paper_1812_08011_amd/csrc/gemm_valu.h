@@ -23,4 +23,9 @@ ValuShape valu_shape(int cfg);
 // for chunk lengths the matrix cores cannot split).
 const void* valu_kernel(int cfg, int ta, int tb, int fast);
 
+// Exact-mode kernel of configuration cfg whose A operand is an implicitly
+// lowered convolution input (GemmArgs::conv); trans_b = 0; null where not
+// built (only configuration 4).
+const void* valu_conv_kernel(int cfg, int ta);
+
 }  // namespace fp8t

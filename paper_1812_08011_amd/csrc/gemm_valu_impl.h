@@ -87,6 +87,60 @@ __device__ __forceinline__ void slab_load(const uint8_t* __restrict__ ptr, int64
     }
 }
 
+// The same for an implicitly lowered convolution input (ConvGeom): the
+// operand is Xcol (KC: element (r, k) = Xcol(r, k), rows are output pixels)
+// or Xcol^T (element (r, k) = Xcol(k, r)).  A word holds 4 consecutive Xcol
+// columns of one pixel: 4 consecutive channels of one input position when
+// C % 4 == 0 (one 4-byte load), otherwise gathered byte by byte.
+__device__ __forceinline__ uint32_t xcol_byte(const uint8_t* __restrict__ X, const ConvGeom& cg,
+                                              int pix, int col) {
+    const int n = pix / cg.OHW, rem = pix - n * cg.OHW;
+    const int oh = rem / cg.OW, ow = rem - oh * cg.OW;
+    const int kh = col / cg.KWC, r2 = col - kh * cg.KWC;
+    const int kw = r2 / cg.C, c = r2 - kw * cg.C;
+    const int ih = oh * cg.stride - cg.pad + kh, iw = ow * cg.stride - cg.pad + kw;
+    if ((unsigned)ih >= (unsigned)cg.H || (unsigned)iw >= (unsigned)cg.W) return 0u;
+    return X[(((int64_t)n * cg.H + ih) * cg.W + iw) * cg.C + c];
+}
+
+template <bool KC, int R, int BK, int NT, int W>
+__device__ __forceinline__ void slab_load_conv(const uint8_t* __restrict__ X, const ConvGeom& cg,
+                                               int r0, int rows, int k0, int kend, int tid,
+                                               uint32_t (&reg)[W]) {
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int d = tid + NT * w;
+        int r, k;
+        if (KC) { r = d / (BK / 4); k = (d % (BK / 4)) * 4; }
+        else    { k = d / (R / 4);  r = (d % (R / 4)) * 4; }
+        const int gr = r0 + r, gk = k0 + k;
+        // pixel and first column of the word; valid columns [col, col + nb)
+        const int pix = KC ? gr : gk, col = KC ? gk : gr;
+        const bool in = gr < rows && gk < kend;
+        const int lim = KC ? kend - gk : rows - gr;
+        const int nb = lim < 4 ? lim : 4;
+        uint32_t v = 0;
+        if (in) {
+            // one 4-byte load when the word is 4 aligned channels of one input
+            // position (chunk ranges need not start at a multiple of 4)
+            if (cg.vec && (col & 3) == 0) {
+                const int n = pix / cg.OHW, rem = pix - n * cg.OHW;
+                const int oh = rem / cg.OW, ow = rem - oh * cg.OW;
+                const int kh = col / cg.KWC, r2 = col - kh * cg.KWC;
+                const int kw = r2 / cg.C, c = r2 - kw * cg.C;
+                const int ih = oh * cg.stride - cg.pad + kh, iw = ow * cg.stride - cg.pad + kw;
+                if ((unsigned)ih < (unsigned)cg.H && (unsigned)iw < (unsigned)cg.W)
+                    v = *reinterpret_cast<const uint32_t*>(
+                        X + (((int64_t)n * cg.H + ih) * cg.W + iw) * cg.C + c);
+                if (nb < 4) v &= (1u << (8 * nb)) - 1u;
+            } else {
+                for (int b = 0; b < nb; ++b) v |= xcol_byte(X, cg, pix, col + b) << (8 * b);
+            }
+        }
+        reg[w] = v;
+    }
+}
+
 // Decode a thread's words into the LDS slab, laid out [k][row] with `pitch`
 // floats per k, each value times 2^SH.  The FP8 codes are the OCP E5M2
 // ("bf8") encoding (bias 15, gradual underflow, exponent 31 for Inf/NaN), so
@@ -127,7 +181,9 @@ __device__ __forceinline__ void slab_store(float* lds, int pitch, int tid,
     }
 }
 
-template <int TM, int TN, int LM, int LN, int BK, bool PF, int WPE, bool TA, bool TB, bool FAST>
+// CONV: the A operand is the implicit lowering of an NHWC input (g.conv).
+template <int TM, int TN, int LM, int LN, int BK, bool PF, int WPE, bool TA, bool TB, bool FAST,
+          bool CONV = false>
 __global__ __launch_bounds__(LM * LN) __attribute__((amdgpu_waves_per_eu(WPE)))
 void chunk_gemm_valu(GemmArgs g, Plan p) {
     constexpr int NT = LM * LN;
@@ -157,6 +213,13 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 
     uint32_t ra[WA], rb[WB];
     float P[TM][TN], S[TM][TN];
+
+    auto load_a = [&](int m0, int k0, int kend) __attribute__((always_inline)) {
+        if (CONV)
+            slab_load_conv<KCA, BM, BK, NT, WA>(g.A, g.conv, m0, g.M, k0, kend, tid, ra);
+        else
+            slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, k0, kend, tid, ra);
+    };
 
     auto lds_read = [&](float (&a)[TM], float (&b)[TN], int buf, int kk) __attribute__((always_inline)) {
 #pragma unroll
@@ -247,7 +310,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         const int nk = kend - kbeg;
         const int nslabs = (nk + BK - 1) / BK;
         int crem = g.CL;                 // products left in the current chunk
-        slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, kbeg, kend, tid, ra);
+        load_a(m0, kbeg, kend);
         slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, kbeg, kend, tid, rb);
         slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[0][0][0], BM + PA, tid, ra, amax_a, special);
         slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[0][0][0], BN + PB, tid, rb, amax_b, special);
@@ -256,7 +319,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             const int buf = s & 1;
             const int ks = kbeg + s * BK;
             if (s + 1 < nslabs) {
-                slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, ks + BK, kend, tid, ra);
+                load_a(m0, ks + BK, kend);
                 slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, ks + BK, kend, tid, rb);
             }
             const int kmax = min(BK, kend - ks);

@@ -37,6 +37,7 @@ def test_header_declares_the_boundary():
         "chunk_gemm_sr", "chunk_gemm_sr_workspace_size", "adam_update",
         "chunk_gemm_p16", "chunk_gemm_p16_workspace_size",
         "relu_codes", "relu_backward_fp8", "mse_grad_fp16",
+        "conv2d_fwd_fp8", "conv2d_wgrad_fp8", "conv2d_workspace_size", "col2im_fp16",
         "sr_weight_update", "fp8t_status_string"])
 
 
@@ -174,6 +175,31 @@ def test_elementwise_rejects(lib):
     assert lib.relu_backward_fp8(FAKE, FAKE, FAKE, -2, 1.0, None) == E
     assert lib.mse_grad_fp16(FAKE, FAKE, None, 4, 1.0, None) == E
     assert lib.mse_grad_fp16(None, None, None, 0, 1.0, None) == fp8t.OK
+
+
+def test_conv_rejects(lib):
+    E = fp8t.EINVAL
+
+    def fwd(**kw):
+        a = dict(X=FAKE, N=2, H=5, W=5, C=4, KH=3, KW=3, pad=1, stride=1, Wt=FAKE, Cout=8, CL=64,
+                 Y=FAKE, ldy=8, ws=None, wsb=0)
+        a.update(kw)
+        return lib.conv2d_fwd_fp8(a["X"], a["N"], a["H"], a["W"], a["C"], a["KH"], a["KW"],
+                                  a["pad"], a["stride"], a["Wt"], a["Cout"], a["CL"], a["Y"],
+                                  a["ldy"], a["ws"], a["wsb"], None)
+    for bad in (dict(N=-1), dict(H=0), dict(C=0), dict(KH=0), dict(stride=0), dict(pad=-1),
+                dict(KH=8), dict(Cout=-1), dict(CL=0), dict(X=None), dict(Wt=None),
+                dict(Y=None), dict(ldy=7), dict(ws=None, wsb=16)):
+        assert fwd(**bad) == E, bad
+    assert fwd(N=0) == fp8t.OK
+    assert fwd(Cout=0) == fp8t.OK
+    assert lib.conv2d_wgrad_fp8(FAKE, 2, 5, 5, 4, 3, 3, 1, 1, FAKE, 8, 64, FAKE, 7, None, 0,
+                                None) == E
+    assert fp8t.conv2d_workspace_size(2, 2, 5, 5, 4, 3, 3, 1, 1, 8, 64) == 0
+    assert fp8t.conv2d_workspace_size(0, 2, 5, 5, 4, 3, 3, 1, 0, 8, 64) == 0
+    assert lib.col2im_fp16(FAKE, 2, 5, 5, 4, 3, 3, 1, 0, FAKE, None) == E
+    assert lib.col2im_fp16(None, 2, 5, 5, 4, 3, 3, 1, 1, FAKE, None) == E
+    assert lib.col2im_fp16(None, 0, 5, 5, 4, 3, 3, 1, 1, None, None) == fp8t.OK
 
 
 def test_workspace_size_without_a_device(lib):

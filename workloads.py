@@ -67,6 +67,19 @@ def im2col_3x3(X):
     return cols
 
 
+def conv_stage_input(seed=2, batch=256, hw=14, cin=256, cout=256):
+    """The conv stage before lowering: X NHWC ~ ReLU(N(0,1)), W (9 cin x cout)
+    ~ N(0, sqrt(2/K)) in (kh, kw, cin) row order, dY (batch hw hw x cout) ~
+    N(0, 1e-3) with a loss scale of 1024 applied by the quantizer -- the same
+    draws as conv_gemms."""
+    rng = np.random.default_rng(seed)
+    X = np.maximum(rng.standard_normal((batch, hw, hw, cin)), 0.0).astype(np.float32)
+    K = 9 * cin
+    W = _normal(rng, (K, cout), np.sqrt(2.0 / K))
+    dY = _normal(rng, (batch * hw * hw, cout), 1e-3)
+    return dict(X=X, W=W, dY=dY, dy_scale=1024.0)
+
+
 def conv_gemms(seed=2, batch=256, hw=14, cin=256, cout=256):
     """Returns dict with Xcol (M x K), W (K x cout), dY (M x cout) as float32
     and the loss scale for dY.
