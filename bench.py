@@ -161,7 +161,9 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
     * adam_update at 25.6 M parameters, against HBM;
     * one whole training step of the speech DNN (440 -> 1024 x 5 -> 6000,
       batch 256; FP8 hidden layers, FP16 last layer, loss scale 1000, SR
-      update) in exact and fast mode."""
+      update) in exact and fast mode;
+    * the conv stage through the implicit lowering (Forward, Gradient) and
+      col2im of its lowered error."""
     out = {}
     sr = {}
     for name, (ta, tb, m_, n_, k_, A, B) in (("fwd", (0, 0, M, N, K, X8, W8)),
@@ -214,7 +216,38 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
                                 "frac_of_hbm": 15 * n / (t * 1e-3) / HBM_BYTES_S}
     del w16, g16, v16, w8, m16, s16
     out["speech_dnn_step"] = mlp_measurement(torch, fp8t)
+    out["conv_implicit"] = conv_measurement(torch, fp8t, W8, D8, u8, u16)
     return out
+
+
+def conv_measurement(torch, fp8t, W8, D8, u8, u16):
+    """The conv stage's Forward and Gradient GEMMs reading the NHWC input
+    directly (no lowered matrix in memory), and col2im of the lowered error."""
+    import workloads
+    st = workloads.conv_stage_input()
+    N, H, W, C = st["X"].shape
+    Cout = st["W"].shape[1]
+    X8 = u8(N, H, W, C)
+    fp8t.fp8_quantize(torch.from_numpy(st["X"]).cuda(), X8)
+    M, K = N * H * W, 9 * C
+    res = {}
+    for wg, name, B, rows in ((0, "fwd", W8, M), (1, "wgrad", D8, K)):
+        wb = fp8t.conv2d_workspace_size(wg, N, H, W, C, 3, 3, 1, 1, Cout, CL)
+        ws = u8(wb) if wb else None
+        out = u16(rows, Cout)
+        f = fp8t.conv2d_wgrad_fp8 if wg else fp8t.conv2d_fwd_fp8
+        t = time_ms(torch, lambda: f(X8, N, H, W, C, 3, 3, 1, 1, B, Cout, CL, out, Cout, ws, wb),
+                    3)
+        res[name] = {"ms": t, "tmac_s": M * K * Cout / (t * 1e-3) / 1e12,
+                     "frac_of_valu_emulation_peak": M * K * Cout / (t * 1e-3) /
+                     exact_peak_mac_s(CL)}
+        del ws, out
+    cols = u16(M, K)
+    fp8t.fp16_quantize(torch.randn(M, K, device="cuda") * 1e-2, cols)
+    dX = u16(N, H, W, C)
+    t = time_ms(torch, lambda: fp8t.col2im_fp16(cols, N, H, W, C, 3, 3, 1, 1, dX), 5)
+    res["col2im"] = {"us": t * 1e3, "gb_s": 2 * (M * K + N * H * W * C) / (t * 1e-3) / 1e9}
+    return res
 
 
 def mlp_measurement(torch, fp8t):
