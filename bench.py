@@ -18,7 +18,7 @@ before timing.  `value` = all chunk_gemm multiply-accumulates of a step
 (3 exact + 3 fast GEMMs) / step time, in GMAC/s.  Per-kernel times come from
 HIP events recorded on the stream the library launches on.
 
-    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extras]
 """
 import argparse
 import json
@@ -97,6 +97,8 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the measurements outside the timed step (profiling runs)")
     p.add_argument("--cpu-seconds", type=float, default=20.0,
                    help="target wall time of the oracle sample")
     return p.parse_args()
@@ -416,7 +418,8 @@ def main():
             "quantize_gb_s": q_bytes / per["quantize"] / 1e9,
         },
     }
-    result["kernels"].update(extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16))
+    if not args.no_extras:
+        result["kernels"].update(extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16))
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(work, args.cpu_seconds)
     print(json.dumps(result), flush=True)
