@@ -46,12 +46,12 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # HBM traffic of the exact-mode chunk_gemm calls of one step, from two
 # rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) over this benchmark,
 # calibrated by the counters of a plain device copy of known size (fetch x2.0,
-# write x1.0); average calibrated bytes per call (forward 197.6 MB,
-# backward-data 257.4 MB, weight-gradient 3072.9 MB including the chunk sums
+# write x1.0); average calibrated bytes per call (forward 196.2 MB,
+# backward-data 257.5 MB, weight-gradient 3072.8 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on: any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "a2b7657ff4af5cbbbcd37b6d1285c6d4d4b6a9dcbe73b3b18ec9ece79bd2ddb5"
-EXACT_TRAFFIC_BYTES_PER_CALL = (197.6e6 + 257.4e6 + 3072.9e6) / 3
+TRAFFIC_SOURCES_SHA256 = "a5738bda7db9dd1a7afdc53746e04b77ee54728883247fcb0e7d2fc02212188b"
+EXACT_TRAFFIC_BYTES_PER_CALL = 1175.5e6
 
 
 def kernel_sources_sha256():
