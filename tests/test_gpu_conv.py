@@ -87,7 +87,8 @@ def test_conv_misaligned_input_takes_byte_loads():
 def test_col2im_small():
     rng = np.random.default_rng(1012)
     for (N, H, W, C, KH, KW, pad, stride) in ((2, 7, 6, 5, 3, 3, 1, 1), (1, 9, 9, 4, 3, 3, 1, 2),
-                                               (3, 5, 8, 2, 2, 3, 0, 1)):
+                                               (3, 5, 8, 2, 2, 3, 0, 1), (2, 6, 7, 16, 3, 3, 1, 1),
+                                               (1, 8, 8, 24, 3, 2, 1, 2)):
         OH, OW = oconv.out_size(H, W, KH, KW, pad, stride)
         g = oracle.fp16_quantize((rng.standard_normal((N * OH * OW, KH * KW * C)) * 100)
                                  .astype(np.float32))
