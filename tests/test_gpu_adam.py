@@ -63,9 +63,12 @@ def test_adam_variants():
     _case(*_state(rng, 20_000), b1=0.5, b2=0.9, eps=1e-4, wd=0.0, lr=0.1)
 
 
-def test_adam_specials():
+@pytest.mark.parametrize("n", [20_001, 4_500_003])
+def test_adam_specials(n):
+    """Special codes among ordinary values: their pairs take the general
+    path, the others the normal-range one (at the larger size every thread of
+    the capped grid loops over several pairs)."""
     rng = np.random.default_rng(961)
-    n = 20_001
     w, g, m, v = _state(rng, n)
     specials = np.uint16([0x0000, 0x8000, 0x0001, 0x81FF, 0x7DFF, 0xFDFF, 0x7E00, 0xFE00,
                           0x7F00, 0xBE00])                     # 0xBE00: -1 (negative v)

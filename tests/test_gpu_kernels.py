@@ -436,8 +436,8 @@ def test_sr_update_mixed_ranges(n):
     """Elements outside FP16's normal range (zeros, subnormals, values whose
     update leaves the range or overflows, Inf, NaN) scattered among ordinary
     ones: the groups holding them take the general path, the others the
-    normal-range one, and both must agree with the oracle (one pair per
-    thread at the smaller size, four at the larger)."""
+    normal-range one, and both must agree with the oracle (at the larger size
+    every thread of the capped grid loops over several pairs)."""
     rng = np.random.default_rng(544)
     w = oracle.fp16_quantize((rng.standard_normal(n) * 0.02).astype(np.float32))
     g = oracle.fp16_quantize((rng.standard_normal(n) * 1e-4).astype(np.float32))
