@@ -46,6 +46,8 @@
 
 #include <stdio.h>
 
+#include <type_traits>
+
 namespace fp8t {
 namespace {
 
@@ -68,6 +70,7 @@ struct TileArgs {
     uint32_t w3;                      // 2 * offset
     int c_vec;                        // C rows allow 8-byte stores of 4 codes
     int a_vec, b_vec;                 // A / B rows allow 8-element loads
+    int guarded;                      // FP16 operands: try the guarded path first
 };
 
 // Uniform-derived addend: (2^14 - 1) - (u >> 2) for the 16-bit uniform in
@@ -102,12 +105,21 @@ __device__ __forceinline__ float fp16_to_f32_shift(uint32_t c) {
 }
 
 // Operand element (code) -> float in the kernel's domain: FP8 A scaled by
-// 2^96, FP8 B plain; FP16 A and B scaled by 2^48 each.
-template <int FMT, bool IS_A>
+// 2^96, FP8 B plain; FP16 A and B scaled by 2^48 each, or plain on the
+// guarded path (PLAIN).
+template <int FMT, bool IS_A, bool PLAIN = false>
 __device__ __forceinline__ float decode(uint32_t c) {
     if (FMT == 8) return IS_A ? fp8_to_f32<96>(c) : fp8_to_f32<0>(c);
-    return fp16_to_f32_shift<48>(c);
+    return PLAIN ? fp16_to_f32(c) : fp16_to_f32_shift<48>(c);
 }
+
+// Operand statistics of a piece on the guarded path: largest magnitude
+// decoded, and whether an Inf/NaN code was seen.
+struct Track {
+    float amax = 0.0f;
+    uint32_t special = 0u;
+    __device__ __forceinline__ void add(float f) { amax = fmaxf(amax, __builtin_fabsf(f)); }
+};
 
 template <int FMT> struct Elem;
 template <> struct Elem<8> { typedef uint8_t t; typedef uint2 v8; };
@@ -116,10 +128,10 @@ template <> struct Elem<16> { typedef uint16_t t; typedef uint4 v8; };
 // Stage a whole slab (64 rows x 32 k, all inside the matrix, aligned rows)
 // with one 8-element load per thread.  KC: k is contiguous in memory
 // (element (r, k) at p[r * ld + k]); otherwise the row index is.
-template <int FMT, bool IS_A, bool KC>
+template <int FMT, bool IS_A, bool KC, bool PLAIN = false>
 __device__ __forceinline__ void stage_fast(const typename Elem<FMT>::t* __restrict__ p,
                                            int64_t ld, int r0, int k0, float (*X)[kPitch],
-                                           int tid) {
+                                           int tid, Track& tr) {
     typedef typename Elem<FMT>::v8 V;
     uint32_t w[FMT / 4];
     float f[8];
@@ -137,7 +149,11 @@ __device__ __forceinline__ void stage_fast(const typename Elem<FMT>::t* __restri
     for (int e = 0; e < 8; ++e) {
         const uint32_t c = FMT == 8 ? (w[e / 4] >> (8 * (e % 4))) & 0xFFu
                                     : (w[e / 2] >> (16 * (e % 2))) & 0xFFFFu;
-        f[e] = decode<FMT, IS_A>(c);
+        f[e] = decode<FMT, IS_A, PLAIN>(c);
+        if (PLAIN) {
+            tr.add(f[e]);
+            tr.special |= (FMT == 16 && ((c >> 9) & 63u) == 63u) ? 1u : 0u;
+        }
     }
     if (KC) {
 #pragma unroll
@@ -156,10 +172,32 @@ __device__ __forceinline__ float round_product16(float p) {
     return __builtin_fabsf(p) < 0x1p66f ? sub : rn16s(p);
 }
 
+// Plain product of two FP16 values (exact in float: at most 20 significant
+// bits, far inside float's exponent range) rounded to FP16, nearest even:
+// adding 1.5 x 2^(E + 14), E = max(exponent of p, -30), puts the last kept
+// bit of p at float's last bit (10 significant bits; a fixed step of 2^-39
+// below 2^-30, FP16's subnormal range), and subtracting it again is exact.
+__device__ __forceinline__ float rn16_product_plain(float p) {
+    uint32_t e = __float_as_uint(p) & 0x7F800000u;
+    e = e > (97u << 23) ? e : (97u << 23);
+    const float magic = __uint_as_float(e + (14u << 23) + 0x00400000u);
+    return (p + magic) - magic;
+}
+
 // FMT: operand format (8 = FP8 codes, 16 = FP16 codes); SR: stochastic
-// rounding of every addition (else nearest).
+// rounding of every addition (else nearest).  FP16 operands with nearest
+// rounding first try a guarded path, like the exact mode of chunk_gemm: plain
+// values, products rounded by rn16_product_plain and sums by Veltkamp
+// splitting (rn16v), valid when no operand is Inf/NaN and no partial sum can
+// reach FP16's overflow threshold (each is at most 9 (1 + 2^-10) K max|a|
+// max|b|, the rounded products being at most (1 + 2^-10) |a b|).  Sums below
+// 2^-30 need no subnormal step there: every term is a multiple of 2^-39, so
+// such a sum is exact in float and already an FP16 value.  A piece that
+// fails is recomputed in the 2^96 domain.
 template <bool TA, bool TB, int FMT, bool SR>
 __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p) {
+    constexpr bool HAS_GUARDED = FMT == 16 && !SR;
+    __shared__ float s_track[3];
     typedef typename Elem<FMT>::t E;
     const E* __restrict__ A = static_cast<const E*>(g.A);
     const E* __restrict__ B = static_cast<const E*>(g.B);
@@ -168,8 +206,16 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
     const int tid = threadIdx.x;
     const int tx = tid % kTiles, ty = tid / kTiles;
 
-    // chunks [c0, c1) of tile; lt >= 0 for a shared tile
-    auto piece = [&](int64_t tile, int c0, int c1, int64_t lt) __attribute__((always_inline)) {
+    // chunks [c0, c1) of tile; lt >= 0 for a shared tile.  Returns false when
+    // the guarded path's check fails (nothing has then been written to C).
+    auto piece = [&](auto guard_tag, int64_t tile, int c0, int c1, int64_t lt)
+                     __attribute__((always_inline)) -> bool {
+        constexpr bool GUARDED = decltype(guard_tag)::value;
+        constexpr int DOM = GUARDED ? 0 : 96;
+        auto rnd = [&](float x) __attribute__((always_inline)) -> float {
+            return GUARDED ? rn16v(x) : rn16s(x);
+        };
+        Track ta, tb;
         const int m0 = (int)(tile / p.tiles_n) * kBM;
         const int n0 = (int)(tile % p.tiles_n) * kBN;
         const int kbeg = (int)((int64_t)c0 * g.CL);
@@ -193,8 +239,10 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
 #pragma unroll
                 for (int r = 0; r < kT; ++r) {
                     uint2 v;
-                    v.x = (uint32_t)f32s_to_fp16(P[r][0]) | ((uint32_t)f32s_to_fp16(P[r][1]) << 16);
-                    v.y = (uint32_t)f32s_to_fp16(P[r][2]) | ((uint32_t)f32s_to_fp16(P[r][3]) << 16);
+                    v.x = (uint32_t)f32d_to_fp16<DOM>(P[r][0]) |
+                          ((uint32_t)f32d_to_fp16<DOM>(P[r][1]) << 16);
+                    v.y = (uint32_t)f32d_to_fp16<DOM>(P[r][2]) |
+                          ((uint32_t)f32d_to_fp16<DOM>(P[r][3]) << 16);
                     *reinterpret_cast<uint2*>(dst + r * kBN) = v;
                 }
             } else if (SR) {
@@ -212,7 +260,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
 #pragma unroll
                 for (int r = 0; r < kT; ++r)
 #pragma unroll
-                    for (int c = 0; c < kT; ++c) S[r][c] = rn16s(S[r][c] + P[r][c]);
+                    for (int c = 0; c < kT; ++c) S[r][c] = rnd(S[r][c] + P[r][c]);
             }
 #pragma unroll
             for (int r = 0; r < kT; ++r)
@@ -230,7 +278,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
             // stage op(A)[m0.., lo..hi) and op(B)[lo..hi), n0..) as floats;
             // rows, columns and k outside are zero
             if (lo == sb && hi == sb + kBK && m0 + kBM <= g.M && g.a_vec) {
-                stage_fast<FMT, true, !TA>(A, g.lda, m0, sb, As, tid);
+                stage_fast<FMT, true, !TA, GUARDED>(A, g.lda, m0, sb, As, tid, ta);
             } else {
 #pragma unroll
                 for (int q = 0; q < kBM * kBK / kNT; ++q) {
@@ -241,11 +289,15 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
                     uint32_t code = 0;
                     if (m < g.M && k >= lo && k < hi)
                         code = TA ? A[(int64_t)k * g.lda + m] : A[(int64_t)m * g.lda + k];
-                    As[kk][mm] = decode<FMT, true>(code);
+                    As[kk][mm] = decode<FMT, true, GUARDED>(code);
+                    if (GUARDED) {
+                        ta.add(As[kk][mm]);
+                        ta.special |= ((code >> 9) & 63u) == 63u ? 1u : 0u;
+                    }
                 }
             }
             if (lo == sb && hi == sb + kBK && n0 + kBN <= g.N && g.b_vec) {
-                stage_fast<FMT, false, TB>(B, g.ldb, n0, sb, Bs, tid);
+                stage_fast<FMT, false, TB, GUARDED>(B, g.ldb, n0, sb, Bs, tid, tb);
             } else {
 #pragma unroll
                 for (int q = 0; q < kBN * kBK / kNT; ++q) {
@@ -256,7 +308,11 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
                     uint32_t code = 0;
                     if (n < g.N && k >= lo && k < hi)
                         code = TB ? B[(int64_t)n * g.ldb + k] : B[(int64_t)k * g.ldb + n];
-                    Bs[kk][nn] = decode<FMT, false>(code);
+                    Bs[kk][nn] = decode<FMT, false, GUARDED>(code);
+                    if (GUARDED) {
+                        tb.add(Bs[kk][nn]);
+                        tb.special |= ((code >> 9) & 63u) == 63u ? 1u : 0u;
+                    }
                 }
             }
             __syncthreads();
@@ -290,16 +346,35 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
                             if (FMT == 8) {
                                 x = __builtin_fmaf(av[r], bv[c], P[r][c]);
                             } else {
-                                x = P[r][c] + round_product16(av[r] * bv[c]);
+                                x = P[r][c] + (GUARDED ? rn16_product_plain(av[r] * bv[c])
+                                                       : round_product16(av[r] * bv[c]));
                             }
                             P[r][c] = SR ? sr16s(x, sr_addend(nw[r][2 * s + c / 2], c % 2))
-                                         : rn16s(x);
+                                         : rnd(x);
                         }
                     if (k + 1 == cend) chunk_end();
                 }
             }
         }
-        if (to_ws) return;
+        if (GUARDED) {
+            // the workgroup's operand statistics of this piece (non-negative
+            // floats compare as their bit patterns)
+            if (tid == 0) s_track[0] = s_track[1] = s_track[2] = 0.0f;
+            __syncthreads();
+            uint32_t* st = reinterpret_cast<uint32_t*>(s_track);
+            atomicMax(&st[0], __float_as_uint(ta.amax));
+            atomicMax(&st[1], __float_as_uint(tb.amax));
+            atomicOr(&st[2], ta.special | tb.special);
+            __syncthreads();
+            const float ma = s_track[0], mb = s_track[1];
+            const uint32_t sp = st[2];
+            __syncthreads();               // s_track is reused by the next piece
+            if (sp) return false;
+            // the bound uses the full K, so that pieces of one tile that each
+            // pass bound the whole chain together
+            if (!(9.01 * (double)g.K * (double)ma * (double)mb < 2147483648.0)) return false;
+        }
+        if (to_ws) return true;
         // the running sum: the result of a whole tile, or the start of a
         // shared tile's chain (continued by chunk_fold_tile)
 #pragma unroll
@@ -309,19 +384,30 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
             uint16_t* cp = g.C + (int64_t)m * g.ldc + n;
             if (g.c_vec && n + kT <= g.N) {
                 uint2 v;
-                v.x = (uint32_t)f32s_to_fp16(S[r][0]) | ((uint32_t)f32s_to_fp16(S[r][1]) << 16);
-                v.y = (uint32_t)f32s_to_fp16(S[r][2]) | ((uint32_t)f32s_to_fp16(S[r][3]) << 16);
+                v.x = (uint32_t)f32d_to_fp16<DOM>(S[r][0]) |
+                      ((uint32_t)f32d_to_fp16<DOM>(S[r][1]) << 16);
+                v.y = (uint32_t)f32d_to_fp16<DOM>(S[r][2]) |
+                      ((uint32_t)f32d_to_fp16<DOM>(S[r][3]) << 16);
                 *reinterpret_cast<uint2*>(cp) = v;
             } else {
 #pragma unroll
                 for (int c = 0; c < kT; ++c)
-                    if (n + c < g.N) cp[c] = f32s_to_fp16(S[r][c]);
+                    if (n + c < g.N) cp[c] = f32d_to_fp16<DOM>(S[r][c]);
             }
         }
+        return true;
+    };
+
+    auto run = [&](int64_t tile, int c0, int c1, int64_t lt) __attribute__((always_inline)) {
+        bool done = false;
+        if constexpr (HAS_GUARDED) {
+            if (g.guarded) done = piece(std::integral_constant<bool, true>{}, tile, c0, c1, lt);
+        }
+        if (!done) piece(std::integral_constant<bool, false>{}, tile, c0, c1, lt);
     };
 
     const int w = blockIdx.x;
-    for (int64_t t = w; t < p.t_whole; t += p.G) piece(whole_tile(p, t), 0, p.nch, -1);
+    for (int64_t t = w; t < p.t_whole; t += p.G) run(whole_tile(p, t), 0, p.nch, -1);
     if (p.L > 0) {
         int64_t s = (int64_t)w * p.L / p.G;
         const int64_t e = (int64_t)(w + 1) * p.L / p.G;
@@ -330,7 +416,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
             const int c0 = (int)(s - lt * p.nch);
             const int64_t c1l = e - lt * p.nch;
             const int c1 = c1l < p.nch ? (int)c1l : p.nch;
-            piece(p.t_whole + lt, c0, c1, lt);
+            run(p.t_whole + lt, c0, c1, lt);
             s = lt * p.nch + c1;
         }
     }
@@ -501,6 +587,8 @@ int tile_call(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, const
     const int eb = FMT / 8;                   // bytes per element
     g.a_vec = aligned(A, 8 * eb) && lda % 8 == 0;
     g.b_vec = aligned(B, 8 * eb) && ldb % 8 == 0;
+    // FP8T_GEMM_GUARD=0 runs every piece on the 2^96-domain path (tests)
+    g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
     Plan plan = tp.plan;
     void* args[] = {&g, &plan};
     if (hipLaunchKernel(fn, dim3(plan.G), dim3(kNT), args, 0, stream) != hipSuccess)

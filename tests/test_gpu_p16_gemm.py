@@ -38,9 +38,11 @@ SHAPES = [(130, 67, 333, 64), (64, 96, 1000, 7), (33, 47, 700, 700), (70, 150, 6
           (5, 3, 17, 4), (128, 64, 2048, 64)]
 
 
+@pytest.mark.parametrize("guard", ["1", "0"])
 @pytest.mark.parametrize("plan", ["auto", "shared", "no_ws"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
-def test_p16_gemm_matches_oracle(ta, tb, plan, monkeypatch):
+def test_p16_gemm_matches_oracle(ta, tb, plan, guard, monkeypatch):
+    monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
     if plan == "shared":
         monkeypatch.setenv("FP8T_GEMM_SPLIT", "1")
         monkeypatch.setenv("FP8T_GEMM_WGS", "7")
@@ -50,13 +52,18 @@ def test_p16_gemm_matches_oracle(ta, tb, plan, monkeypatch):
         b = rng.standard_normal((K, N)) * 0.5
         a[rng.random(a.shape) < 0.03] = 0.0
         A, B = p16(a.T if ta else a), p16(b.T if tb else b)
-        say(f"chunk_gemm_p16 plan={plan} ta={ta} tb={tb} {M}x{N}x{K} CL={CL}")
+        say(f"chunk_gemm_p16 plan={plan} guard={guard} ta={ta} tb={tb} {M}x{N}x{K} CL={CL}")
         got = gemm16(dev(A), dev(B), M, N, K, CL, ta, tb, use_ws=plan != "no_ws")
         ref = oracle.chunk_gemm_p16(A, B, CL, ta, tb)
         assert np.array_equal(got, ref), (M, N, K, CL, np.argwhere(got != ref)[:5])
 
 
-def test_p16_gemm_ranges_and_specials():
+@pytest.mark.parametrize("guard", ["1", "0"])
+def test_p16_gemm_ranges_and_specials(guard, monkeypatch):
+    """Operands whose products leave the guarded path's range (overflowing
+    products, Inf, NaN): the pieces fall back and must still match; with
+    guard 0 every piece runs on the 2^96-domain path."""
+    monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
     rng = np.random.default_rng(985)
     M, N, K, CL = 70, 40, 256, 64
     # magnitudes from 2^-39 to 2^31: subnormal and overflowing products
@@ -68,6 +75,39 @@ def test_p16_gemm_ranges_and_specials():
     A[5, :] = 0x0001                      # smallest subnormal
     A[6, :] = 0x7DFF                      # largest finite
     say("chunk_gemm_p16 ranges and specials")
+    got = gemm16(dev(A), dev(B), M, N, K, CL, 0, 0)
+    assert np.array_equal(got, oracle.chunk_gemm_p16(A, B, CL))
+
+
+@pytest.mark.parametrize("guard", ["1", "0"])
+def test_p16_gemm_small_magnitudes(guard, monkeypatch):
+    """Magnitudes from 2^-39 to 2^-5 times 2^-20 to 1: most products lie in
+    FP16's subnormal range or underflow to 0, every piece passes the guard."""
+    monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+    rng = np.random.default_rng(986)
+    M, N, K, CL = 90, 70, 300, 32
+    a = np.exp2(rng.uniform(-39, -5, (M, K))) * np.sign(rng.standard_normal((M, K)))
+    b = np.exp2(rng.uniform(-20, 0, (K, N))) * np.sign(rng.standard_normal((K, N)))
+    A, B = p16(a), p16(b)
+    say(f"chunk_gemm_p16 small magnitudes guard={guard}")
+    got = gemm16(dev(A), dev(B), M, N, K, CL, 0, 0)
+    assert np.array_equal(got, oracle.chunk_gemm_p16(A, B, CL))
+
+
+@pytest.mark.parametrize("row_scale", [2.0 ** -28, 2.0 ** 17])
+def test_p16_gemm_guard_rows(row_scale, monkeypatch):
+    """One row of A scaled among ordinary ones.  2^-28: products in FP16's
+    subnormal range, rounded on the guarded path itself.  2^17: only the
+    tiles holding the row fail the overflow bound (shared plan: only their
+    pieces) and are recomputed in the 2^96 domain."""
+    monkeypatch.setenv("FP8T_GEMM_SPLIT", "1")
+    monkeypatch.setenv("FP8T_GEMM_WGS", "9")
+    rng = np.random.default_rng(987)
+    M, N, K, CL = 200, 130, 700, 64
+    A = p16(rng.standard_normal((M, K)))
+    B = p16(rng.standard_normal((K, N)))
+    A[150, :] = p16(rng.standard_normal(K) * row_scale)
+    say(f"chunk_gemm_p16 guard rows scale={row_scale}")
     got = gemm16(dev(A), dev(B), M, N, K, CL, 0, 0)
     assert np.array_equal(got, oracle.chunk_gemm_p16(A, B, CL))
 
