@@ -130,12 +130,13 @@ double valu_ops_per_mac(int cfg) {
 // Matrix-core fast mode, CU time of one output-chunk (the VALU epilogue
 // dominates; the matrix-core share grows with CL) and of the per-tile start
 // (pipeline fill, C stores), measured on the conv-stage GEMMs: 64 x 64 tiles
-// with 64-k slabs, 32 x 32 tiles with 128-k slabs.
+// with 64-k slabs, 32 x 32 tiles with 128-k slabs, and the streamed 64 x 64
+// kernel (fitted to its forward and backward-data times).
 double mfma_cost_per_output_chunk(int cfg, int64_t CL) {
-    const double base = cfg == 0 ? 0.156e-9 : 0.17e-9;
+    const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : 0.099e-9;
     return base * (0.6 + 0.4 * (double)CL / 64.0);
 }
-double mfma_cost_per_tile(int cfg) { return cfg == 0 ? 1.1e-6 : 0.66e-6; }
+double mfma_cost_per_tile(int cfg) { return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : 0.77e-6; }
 
 enum Kind { VALU_EXACT = 0, VALU_FAST = 1, MFMA_FAST = 2 };
 
@@ -207,13 +208,19 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 p.nch = (int)nch;
                 double est;
                 size_t ws = 0;
+                // the streamed kernel writes split tiles' chunk sums as scattered
+                // 2-byte stores: the other kernels are faster there
+                if (split && mf && cfg == 2) continue;
                 if (!split) {
                     const int64_t G = T < gmax ? T : gmax;
                     p.G = (int)G;
                     p.t_whole = T;
                     p.L = 0;
-                    // tiles on the busiest CU
-                    const int64_t per_cu = (T + cus - 1) / cus;
+                    // tiles on the busiest CU; the streamed kernel needs at least
+                    // two workgroups on a CU to overlap its matrix-core, vector and
+                    // memory work (a lone one runs at about half the CU rate)
+                    int64_t per_cu = (T + cus - 1) / cus;
+                    if (mf && cfg == 2 && per_cu < 2) per_cu = 2;
                     est = (double)per_cu * (nch * t_chunk + t_tile);
                 } else {
                     int64_t G = gmax;
@@ -355,6 +362,8 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     // also keeps per-thread offsets within a slab in 32 bits
     g.a_vec = aligned(A, 4) && lda % 4 == 0 && lda < (1 << 24);
     g.b_vec = aligned(B, 4) && ldb % 4 == 0 && ldb < (1 << 24);
+    g.a_vec16 = aligned(A, 16) && lda % 16 == 0;
+    g.b_vec16 = aligned(B, 16) && ldb % 16 == 0;
     g.c_vec = C && aligned(C, 4) && ldc % 2 == 0;
     g.c_vec16 = C && aligned(C, 16) && ldc % 8 == 0;
     g.c8_vec8 = C8 && aligned(C8, 8) && ldc8 % 8 == 0;

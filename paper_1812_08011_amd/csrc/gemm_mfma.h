@@ -15,12 +15,15 @@ struct MfmaShape {
     int BK;         // k per LDS slab
 };
 
-constexpr int kMfmaConfigs = 2;
+constexpr int kMfmaConfigs = 3;
 
 MfmaShape mfma_shape(int cfg);
 
 // __global__ function of configuration cfg (0 .. kMfmaConfigs-1) for the
 // given operand layouts, taking (GemmArgs, Plan).
 const void* mfma_kernel(int cfg, int ta, int tb);
+
+// The streamed 64 x 64 kernel (gemm_mfma_stream.hip), configuration 2.
+const void* mfma_stream_kernel(int ta, int tb);
 
 }  // namespace fp8t

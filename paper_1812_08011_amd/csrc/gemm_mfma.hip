@@ -469,6 +469,7 @@ const void* kernel_sel(int ta, int tb) {
 MfmaShape mfma_shape(int cfg) {
     switch (cfg) {
         case 0: return MfmaShape{32, 64, 64, kNT, 16, 64};
+        case 2: return MfmaShape{32, 64, 64, kNT, 64, 64};      // CL a multiple of 64
         default: return MfmaShape{16, 32, 32, kNT, 32, 128};
     }
 }
@@ -477,6 +478,7 @@ const void* mfma_kernel(int cfg, int ta, int tb) {
     switch (cfg) {
         case 0: return kernel_sel<32, 1, 1, 2, 64>(ta, tb);
         case 1: return kernel_sel<16, 1, 1, 2, 128>(ta, tb);
+        case 2: return mfma_stream_kernel(ta, tb);
         default: return nullptr;
     }
 }

@@ -51,6 +51,8 @@ struct GemmArgs {
     int M, N, K, CL;
     int a_vec;          // A, lda allow 4-byte loads (and lda < 2^24)
     int b_vec;          // B, ldb allow 4-byte loads (and ldb < 2^24)
+    int a_vec16;        // A, lda allow 16-byte loads
+    int b_vec16;        // B, ldb allow 16-byte loads
     int c_vec;          // C, ldc allow 4-byte stores of code pairs
     int c_vec16;        // C, ldc allow 16-byte stores (8 codes)
     int c8_vec8;        // C8, ldc8 allow 8-byte stores

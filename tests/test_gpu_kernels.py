@@ -237,7 +237,7 @@ def test_chunk_gemm_workspace_contract():
         assert np.array_equal(host(C), Co)
 
 
-@pytest.mark.parametrize("mtile", ["auto", "0", "1"])
+@pytest.mark.parametrize("mtile", ["auto", "0", "1", "2"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
     """Fast mode against the fast oracle within the derived tolerance, for
@@ -263,7 +263,7 @@ def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
             assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, ta, tb))
 
 
-@pytest.mark.parametrize("mtile", ["0", "1"])
+@pytest.mark.parametrize("mtile", ["0", "1", "2"])
 @pytest.mark.parametrize("wgs", ["2", "9"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (1, 0), (0, 1)])
 def test_chunk_gemm_fast_shared_tiles(mtile, wgs, ta, tb, monkeypatch):
@@ -367,6 +367,37 @@ def test_chunk_gemm_guard_falls_back_per_piece(monkeypatch):
             say(f"guard fallback split={split} wgs={wgs}")
             Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
             assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
+
+
+@pytest.mark.parametrize("mtile", ["0", "1", "2"])
+@pytest.mark.parametrize("wgs", ["0", "1"])
+def test_chunk_gemm_fast_guard_falls_back(mtile, wgs, monkeypatch):
+    """Fast mode: pieces whose chunk sums reach 2^32 are recomputed on the
+    safe epilogue and give the bits of an all-safe run -- a few failing tiles
+    among passing ones, and (one workgroup, every one of its 121 tiles
+    failing) more failures than a workgroup remembers."""
+    monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
+    monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
+    rng = np.random.default_rng(575)
+    M, N, K, CL = 700, 650, 640, 64
+    for case in ("some", "all"):
+        A, B = _operands(rng, M, N, K, 0, 0)
+        if case == "some":
+            A[5, :] = 0x7B                  # 57344
+            B[:, 300] = np.where(rng.random(K) < 0.5, 0x7A, 0xFA)   # +-49152
+        else:
+            A[:, :2] = 0x7B                 # first chunk of every output > 2^32
+            B[:2, :] = 0x7B
+        Ad, Bd = dev(A), dev(B)
+        say(f"fast guard fallback mtile={mtile} wgs={wgs} case={case}")
+        monkeypatch.setenv("FP8T_GEMM_GUARD", "1")
+        Cg = host(gemm(Ad, Bd, M, N, K, CL, mode=fp8t.FAST))
+        monkeypatch.setenv("FP8T_GEMM_GUARD", "0")
+        Cs = host(gemm(Ad, Bd, M, N, K, CL, mode=fp8t.FAST))
+        assert np.array_equal(Cg, Cs), np.argwhere(Cg != Cs)[:5]
+        if case == "all":
+            assert np.all(Cg == 0x7E00)
+            assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, mode=oracle.FAST))
 
 
 @pytest.mark.parametrize("guard", ["1", "0"])
