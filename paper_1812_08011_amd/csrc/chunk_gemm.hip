@@ -54,8 +54,10 @@ __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, in
     if (lt * p.nch >= p.L) return;
     const int local = (int)(idx - lt * per);
     const int64_t tile = p.t_whole + lt;
-    const int m = (int)(tile / p.tiles_n) * BM + local / BN;
-    const int n0 = (int)(tile % p.tiles_n) * BN + local % BN;
+    int tr, tc;
+    tile_rc(p, tile, tr, tc);
+    const int m = tr * BM + local / BN;
+    const int n0 = tc * BN + local % BN;
     if (m >= g.M || n0 >= g.N) return;
     const int a = first_piece_end(p, lt);
     // a tile whose first piece took every chunk needs only its FP8 result

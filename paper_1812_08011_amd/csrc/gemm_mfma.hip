@@ -206,8 +206,10 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                      __attribute__((always_inline)) -> bool {
         constexpr bool SAFE = decltype(safe_tag)::value;
         constexpr int DOM = SAFE ? 96 : 0;
-        const int m0 = (int)(tile / p.tiles_n) * BM;
-        const int n0 = (int)(tile % p.tiles_n) * BN;
+        int tr, tc;
+        tile_rc(p, tile, tr, tc);
+        const int m0 = tr * BM;
+        const int n0 = tc * BN;
         const int kbeg = (int)((int64_t)c0 * g.CL);
         const int64_t kend64 = (int64_t)c1 * g.CL;
         const int kend = kend64 < g.K ? (int)kend64 : g.K;

@@ -150,9 +150,10 @@ struct Work {
         } else {
             return false;
         }
-        const int64_t tm = it.tile / p.tiles_n;
-        it.m0 = (int)tm * kB;
-        it.n0 = (int)(it.tile - tm * p.tiles_n) * kB;
+        int tr, tc;
+        tile_rc(p, it.tile, tr, tc);
+        it.m0 = tr * kB;
+        it.n0 = tc * kB;
         it.kbeg = (int)((int64_t)it.c0 * g.CL);
         const int64_t ke = (int64_t)it.c1 * g.CL;
         it.kend = ke < g.K ? (int)ke : g.K;

@@ -79,6 +79,22 @@ __host__ __device__ inline int64_t whole_tile(const Plan& p, int64_t t) {
     return (t % 8) * (p.t_whole / 8) + t / 8;
 }
 
+// Row and column of tile `tile` in the row-major tile grid.  The tile index
+// of any output that fits in device memory is below 2^32, where a 32-bit
+// division is a fraction of the 64-bit instruction sequence (a per-tile cost
+// on the scalar unit); the 64-bit form stays for the rest.
+__host__ __device__ inline void tile_rc(const Plan& p, int64_t tile, int& tr, int& tc) {
+    if ((uint64_t)tile < (1ull << 32) && (uint64_t)p.tiles_n < (1ull << 32)) {
+        const uint32_t t = (uint32_t)tile, n = (uint32_t)p.tiles_n, q = t / n;
+        tr = (int)q;
+        tc = (int)(t - q * n);
+    } else {
+        const int64_t q = tile / p.tiles_n;
+        tr = (int)q;
+        tc = (int)(tile - q * p.tiles_n);
+    }
+}
+
 // First chunk of shared tile lt that the workspace holds: the end of the
 // piece that starts at the tile's chunk 0 (nch if the tile is not split).
 __host__ __device__ inline int first_piece_end(const Plan& p, int64_t lt) {

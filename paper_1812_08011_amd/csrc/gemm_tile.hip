@@ -197,7 +197,11 @@ __device__ __forceinline__ float rn16_product_plain(float p) {
 template <bool TA, bool TB, int FMT, bool SR>
 __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p) {
     constexpr bool HAS_GUARDED = FMT == 16 && !SR;
-    __shared__ float s_track[3];
+    // |a| max bits, |b| max bits, specials of the guarded pieces, in two slots
+    // used by alternate pieces
+    __shared__ uint32_t s_track[2][3];
+    int gslot = 0;
+    if (threadIdx.x < 6) (&s_track[0][0])[threadIdx.x] = 0;   // ordered by the first slab's barrier
     typedef typename Elem<FMT>::t E;
     const E* __restrict__ A = static_cast<const E*>(g.A);
     const E* __restrict__ B = static_cast<const E*>(g.B);
@@ -216,8 +220,10 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
             return GUARDED ? rn16v(x) : rn16s(x);
         };
         Track ta, tb;
-        const int m0 = (int)(tile / p.tiles_n) * kBM;
-        const int n0 = (int)(tile % p.tiles_n) * kBN;
+        int tr, tc;
+        tile_rc(p, tile, tr, tc);
+        const int m0 = tr * kBM;
+        const int n0 = tc * kBN;
         const int kbeg = (int)((int64_t)c0 * g.CL);
         const int64_t kend64 = (int64_t)c1 * g.CL;
         const int kend = kend64 < g.K ? (int)kend64 : g.K;
@@ -357,18 +363,35 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
             }
         }
         if (GUARDED) {
-            // the workgroup's operand statistics of this piece (non-negative
-            // floats compare as their bit patterns)
-            if (tid == 0) s_track[0] = s_track[1] = s_track[2] = 0.0f;
+            // The workgroup's operand statistics of this piece, reduced within
+            // each wave, then one LDS atomic per wave (non-negative floats
+            // compare as their bit patterns).  Slot gslot was cleared during the
+            // previous guarded piece and is read after the one barrier here;
+            // the other slot, cleared now, is next written after at least one
+            // more barrier (every piece has a slab).
+            uint32_t* st = s_track[gslot];
+            uint32_t ua = __float_as_uint(ta.amax), ub = __float_as_uint(tb.amax);
+            uint32_t us = ta.special | tb.special;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) {
+                ua = max(ua, (uint32_t)__shfl_xor((int)ua, o));
+                ub = max(ub, (uint32_t)__shfl_xor((int)ub, o));
+                us |= (uint32_t)__shfl_xor((int)us, o);
+            }
+            if ((tid & 63) == 0) {
+                atomicMax(&st[0], ua);
+                atomicMax(&st[1], ub);
+                atomicOr(&st[2], us);
+            }
+            if (tid == 0) {
+                s_track[gslot ^ 1][0] = 0;
+                s_track[gslot ^ 1][1] = 0;
+                s_track[gslot ^ 1][2] = 0;
+            }
             __syncthreads();
-            uint32_t* st = reinterpret_cast<uint32_t*>(s_track);
-            atomicMax(&st[0], __float_as_uint(ta.amax));
-            atomicMax(&st[1], __float_as_uint(tb.amax));
-            atomicOr(&st[2], ta.special | tb.special);
-            __syncthreads();
-            const float ma = s_track[0], mb = s_track[1];
+            const float ma = __uint_as_float(st[0]), mb = __uint_as_float(st[1]);
             const uint32_t sp = st[2];
-            __syncthreads();               // s_track is reused by the next piece
+            gslot ^= 1;
             if (sp) return false;
             // the bound uses the full K, so that pieces of one tile that each
             // pass bound the whole chain together
@@ -438,8 +461,10 @@ __global__ __launch_bounds__(256) void chunk_fold_tile(TileArgs g, Plan p) {
     if (lt * p.nch >= p.L) return;
     const int local = (int)(idx - lt * per);
     const int64_t tile = p.t_whole + lt;
-    const int m = (int)(tile / p.tiles_n) * kBM + local / kBN;
-    const int n0 = (int)(tile % p.tiles_n) * kBN + local % kBN;
+    int tr, tc;
+    tile_rc(p, tile, tr, tc);
+    const int m = tr * kBM + local / kBN;
+    const int n0 = tc * kBN + local % kBN;
     if (m >= g.M || n0 >= g.N) return;
     const int a = first_piece_end(p, lt);
     if (a >= p.nch) return;

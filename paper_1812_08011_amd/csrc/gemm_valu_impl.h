@@ -206,13 +206,17 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 
     __shared__ __attribute__((aligned(16))) float As[2][BK][BM + PA];
     __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + PB];
-    __shared__ uint32_t s_track[3];     // |a| max bits, |b| max bits, specials
+    // |a| max bits, |b| max bits, specials of the guarded pieces, in two slots
+    // used by alternate pieces
+    __shared__ uint32_t s_track[2][3];
 
     const int tid = threadIdx.x;
     const int ly = tid / LN, lx = tid % LN;
 
     uint32_t ra[WA], rb[WB];
     float P[TM][TN], S[TM][TN];
+    int gslot = 0;
+    if (tid < 6) (&s_track[0][0])[tid] = 0;    // ordered by the first slab's barrier
 
     auto load_a = [&](int m0, int k0, int kend) __attribute__((always_inline)) {
         if (CONV)
@@ -242,8 +246,10 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         constexpr int ASHIFT = FAST ? 0 : DOM;
         constexpr bool TRACK = !SAFE;
 
-        const int m0 = (int)(tile / p.tiles_n) * BM;
-        const int n0 = (int)(tile % p.tiles_n) * BN;
+        int tr, tc;
+        tile_rc(p, tile, tr, tc);
+        const int m0 = tr * BM;
+        const int n0 = tc * BN;
         const int kbeg = (int)((int64_t)c0 * g.CL);
         const int64_t kend64 = (int64_t)c1 * g.CL;
         const int kend = kend64 < g.K ? (int)kend64 : g.K;
@@ -368,18 +374,35 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         if (crem != g.CL) flush();       // the last, shorter chunk
 
         if (!SAFE) {
-            // Largest magnitudes over the workgroup's operands of this piece.
-            // The bound uses the full K, so that pieces of one tile that each
-            // pass bound the whole chain together.
-            if (tid == 0) { s_track[0] = 0; s_track[1] = 0; s_track[2] = 0; }
+            // Largest magnitudes over the workgroup's operands of this piece
+            // (reduced within each wave, then one LDS atomic per wave).  The
+            // bound uses the full K, so that pieces of one tile that each pass
+            // bound the whole chain together.  Slot `gslot` was cleared during
+            // the previous guarded piece and is read after the one barrier
+            // here; the other slot, cleared now, is next written after at
+            // least one more barrier (every piece has a slab).
+            uint32_t* st = s_track[gslot];
+            uint32_t ua = __float_as_uint(amax_a), ub = __float_as_uint(amax_b), us = special;
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) {      // non-negative floats: bit order
+                ua = max(ua, (uint32_t)__shfl_xor((int)ua, o));
+                ub = max(ub, (uint32_t)__shfl_xor((int)ub, o));
+                us |= (uint32_t)__shfl_xor((int)us, o);
+            }
+            if ((tid & 63) == 0) {
+                atomicMax(&st[0], ua);
+                atomicMax(&st[1], ub);
+                atomicOr(&st[2], us);
+            }
+            if (tid == 0) {
+                s_track[gslot ^ 1][0] = 0;
+                s_track[gslot ^ 1][1] = 0;
+                s_track[gslot ^ 1][2] = 0;
+            }
             __syncthreads();
-            atomicMax(&s_track[0], __float_as_uint(amax_a));   // non-negative: bit order
-            atomicMax(&s_track[1], __float_as_uint(amax_b));
-            atomicOr(&s_track[2], special);
-            __syncthreads();
-            const float ma = __uint_as_float(s_track[0]), mb = __uint_as_float(s_track[1]);
-            const uint32_t sp = s_track[2];
-            __syncthreads();                 // s_track is reused by the next piece
+            const float ma = __uint_as_float(st[0]), mb = __uint_as_float(st[1]);
+            const uint32_t sp = st[2];
+            gslot ^= 1;
             if (sp) return false;                                   // Inf or NaN operand
             const double bound = 9.0 * (double)g.K * (double)ma * (double)mb;
             if (!(bound < 2147483648.0)) return false;             // 2^31
@@ -436,25 +459,30 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
     int64_t t = w;
     int64_t s = p.L > 0 ? (int64_t)w * p.L / p.G : 0;
     const int64_t e = p.L > 0 ? (int64_t)(w + 1) * p.L / p.G : 0;
-    for (;;) {
-        int64_t tile, lt;
-        int c0, c1;
+    auto fetch = [&](int64_t& tile, int64_t& lt, int& c0, int& c1)
+                     __attribute__((always_inline)) -> bool {
         if (t < p.t_whole) {
             tile = whole_tile(p, t);
             lt = -1;
             c0 = 0;
             c1 = p.nch;
             t += p.G;
-        } else if (s < e) {
+            return true;
+        }
+        if (s < e) {
             lt = s / p.nch;
             c0 = (int)(s - lt * p.nch);
             const int64_t c1l = e - lt * p.nch;
             c1 = c1l < p.nch ? (int)c1l : p.nch;
             tile = p.t_whole + lt;
             s = lt * p.nch + c1;
-        } else {
-            break;
+            return true;
         }
+        return false;
+    };
+    int64_t tile, lt;
+    int c0, c1;
+    while (fetch(tile, lt, c0, c1)) {
         bool done = false;
         if (HAS_GUARDED && g.guarded)
             done = piece(std::integral_constant<bool, false>{}, tile, c0, c1, lt);
