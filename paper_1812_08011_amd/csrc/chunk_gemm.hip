@@ -9,6 +9,8 @@
 //   for chunk lengths the matrix cores cannot split;
 // * chunk_gemm_mfma (gemm_mfma.hip) -- the fast mode for CL a multiple of the
 //   MFMA instruction's K (16).
+#include <type_traits>
+
 #include "fp8t_device.h"
 #include "fp8train.h"
 #include "fp8t_host.h"
@@ -43,9 +45,19 @@ __device__ __forceinline__ float fp16_to_f32s_fold(uint32_t c) {
 // continues their running sums, held in C (the FP16 sums of the tile's first
 // piece), over the chunk sums the other pieces left in the workspace, in
 // ascending chunk order -- the same additions a whole-tile pass makes after
-// its first piece.  The chunk sums of kFoldV outputs are one 16-byte load per
-// chunk, issued kFoldU chunks ahead.
-constexpr int kFoldV = 8, kFoldU = 4;
+// its first piece.  The chunk sums of kFoldV outputs are one 2 kFoldV-byte
+// load per chunk, in batches of kFoldU chunks with the next batch in flight
+// while one is added (a split GEMM has few shared outputs and many chunks, so
+// the pass needs many loads in flight per thread; 4 outputs x 16 chunks was
+// the fastest of 4/8 x 16/32 on the conv stage's weight-gradient GEMM).
+#ifndef FP8T_FOLD_V
+#define FP8T_FOLD_V 4
+#endif
+#ifndef FP8T_FOLD_U
+#define FP8T_FOLD_U 16
+#endif
+constexpr int kFoldV = FP8T_FOLD_V, kFoldU = FP8T_FOLD_U;
+typedef std::conditional<kFoldV == 8, uint4, uint2>::type FoldVec;
 
 __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, int BN) {
     const int64_t per = (int64_t)BM * BN;
@@ -69,23 +81,45 @@ __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, in
     float S[kFoldV];
 #pragma unroll
     for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fp16_to_f32s_fold(sp[v]) : 0.0f;
-    const uint4* src = reinterpret_cast<const uint4*>(g.ws + lt * p.nch * per + local);
-    const int64_t step = per / kFoldV;          // uint4 elements per chunk
-    auto add = [&](uint4 q) __attribute__((always_inline)) {
-        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    const FoldVec* src = reinterpret_cast<const FoldVec*>(g.ws + lt * p.nch * per + local);
+    const int64_t step = per / kFoldV;          // vectors per chunk
+    auto add = [&](FoldVec q) __attribute__((always_inline)) {
+        uint32_t w[kFoldV / 2];
+        __builtin_memcpy(w, &q, sizeof(q));
 #pragma unroll
         for (int v = 0; v < kFoldV; ++v)
             S[v] = rn16s(S[v] + fp16_to_f32s_fold((w[v / 2] >> (16 * (v % 2))) & 0xFFFFu));
     };
-    int c = a;
-    for (; c + kFoldU <= p.nch; c += kFoldU) {
-        uint4 q[kFoldU];
+    // two batches of kFoldU chunks: one in flight while the other is added
+    auto load = [&](FoldVec (&q)[kFoldU], int c0) __attribute__((always_inline)) {
+        if (c0 + kFoldU <= p.nch) {
 #pragma unroll
-        for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)(c + u) * step];
+            for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)(c0 + u) * step];
+        } else {
 #pragma unroll
-        for (int u = 0; u < kFoldU; ++u) add(q[u]);
+            for (int u = 0; u < kFoldU; ++u)
+                if (c0 + u < p.nch) q[u] = src[(int64_t)(c0 + u) * step];
+        }
+    };
+    auto fold = [&](const FoldVec (&q)[kFoldU], int c0) __attribute__((always_inline)) {
+        if (c0 + kFoldU <= p.nch) {
+#pragma unroll
+            for (int u = 0; u < kFoldU; ++u) add(q[u]);
+        } else {
+#pragma unroll
+            for (int u = 0; u < kFoldU; ++u)
+                if (c0 + u < p.nch) add(q[u]);
+        }
+    };
+    FoldVec q0[kFoldU], q1[kFoldU];
+    load(q0, a);
+    for (int c = a; c < p.nch; c += 2 * kFoldU) {
+        if (c + kFoldU < p.nch) load(q1, c + kFoldU);
+        fold(q0, c);
+        if (c + kFoldU >= p.nch) break;
+        if (c + 2 * kFoldU < p.nch) load(q0, c + 2 * kFoldU);
+        fold(q1, c + kFoldU);
     }
-    for (; c < p.nch; ++c) add(src[(int64_t)c * step]);
 #pragma unroll
     for (int v = 0; v < kFoldV; ++v) {
         if (v >= nv) continue;
