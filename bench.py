@@ -131,10 +131,35 @@ def cpu_baseline(work, target_s):
     macs, t = run(16)                                     # calibrate
     npts = int(max(16, min(400000, 16 * target_s / max(t, 1e-3))))
     macs, t = run(npts)
-    return {"value": macs / t / 1e9, "unit": "GMAC/s", "cores": oracle.num_threads(),
+    cores = oracle.num_threads()
+    # the same on one core, over a sample sized to take about half as long
+    oracle.set_threads(1)
+    try:
+        n1 = int(max(16, npts * min(1.0, 0.5 / cores)))
+        macs1, t1 = run(n1)
+    finally:
+        oracle.set_threads(cores)
+    return {"value": macs / t / 1e9, "unit": "GMAC/s", "cores": cores,
             "kind": "oracle",
             "sample": f"exact mode, CL {CL}: {npts} sampled outputs of each of the forward, "
-                      f"backward and gradient GEMMs ({macs / 1e6:.0f} M MAC, {t:.1f} s)"}
+                      f"backward and gradient GEMMs ({macs / 1e6:.0f} M MAC, {t:.1f} s)",
+            "single_core": {"value": macs1 / t1 / 1e9, "unit": "GMAC/s",
+                            "sample": f"{n1} sampled outputs of each GEMM ({macs1 / 1e6:.0f} M MAC, "
+                                      f"{t1:.1f} s)"},
+            "host_cpu": host_cpu_model()}
+
+
+def host_cpu_model():
+    """Model name of the host CPU (from /proc/cpuinfo), for the oracle's
+    timing."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def time_ms(torch, fn, reps):

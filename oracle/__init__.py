@@ -93,6 +93,8 @@ def lib():
         L.orc_adam_step_size.argtypes = [f32, f32, f32, u64]
         L.orc_num_threads.restype = ctypes.c_int
         L.orc_num_threads.argtypes = []
+        L.orc_set_threads.restype = None
+        L.orc_set_threads.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
 
@@ -318,3 +320,8 @@ def adam_step_size(lr, beta1, beta2, t):
 
 def num_threads():
     return lib().orc_num_threads()
+
+
+def set_threads(n):
+    """Threads of the oracle's OpenMP loops from now on (n >= 1)."""
+    lib().orc_set_threads(int(n))

@@ -19,6 +19,16 @@ int orc_num_threads(void) {
 #endif
 }
 
+/* Threads used by the OpenMP loops from now on (n >= 1); for timing the
+ * oracle on one core beside the all-core run. */
+void orc_set_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ---- operand quantization ------------------------------------------------
  * Sec. 2.1: weights, activations, errors and gradients are held in FP8 for
  * all GEMMs.  The rounding into P8 is round-to-nearest-even (the paper names

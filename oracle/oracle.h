@@ -109,6 +109,7 @@ int cpu_col2im(const uint16_t* cols, int64_t N, int64_t H, int64_t W, int64_t C,
 
 /* Number of OpenMP threads the oracle's parallel loops use. */
 int orc_num_threads(void);
+void orc_set_threads(int n);
 
 #ifdef __cplusplus
 }
