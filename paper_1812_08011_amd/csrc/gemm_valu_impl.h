@@ -264,6 +264,12 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         auto chunk_value = [&](float x) __attribute__((always_inline)) -> float {
             return FAST ? rn16s(x * 0x1p96f) : x;
         };
+        auto first_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) P[i][j] = __builtin_fmaf(a[i], b[j], 0.0f);
+        };
         auto fma_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
@@ -333,13 +339,19 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             while (kk < kmax) {
                 const int seg = min(kmax - kk, crem);
                 if (seg == BK) {
+                    // A slab that starts a chunk begins with a product into a
+                    // zero partial sum, exact and already an FP16 value (at
+                    // most 6 significant bits, well inside the range): one
+                    // fma with 0 (which also turns -0 into +0) and no rounding.
+                    const bool fresh = crem == g.CL;
                     if (PF) {
                         float a0[TM], b0[TN], a1[TM], b1[TN];
                         lds_read(a0, b0, buf, 0);
 #pragma unroll
                         for (int q = 0; q < BK; q += 2) {
                             lds_read(a1, b1, buf, q + 1);
-                            fma_step(a0, b0);
+                            if (q == 0 && fresh) first_step(a0, b0);
+                            else fma_step(a0, b0);
                             if (q + 2 < BK) lds_read(a0, b0, buf, q + 2);
                             fma_step(a1, b1);
                         }
@@ -348,7 +360,8 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                         for (int q = 0; q < BK; ++q) {
                             float a[TM], b[TN];
                             lds_read(a, b, buf, q);
-                            fma_step(a, b);
+                            if (q == 0 && fresh) first_step(a, b);
+                            else fma_step(a, b);
                         }
                     }
                 } else {
