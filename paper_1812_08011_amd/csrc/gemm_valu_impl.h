@@ -312,11 +312,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 #pragma unroll
                     for (int j = 0; j < TN; ++j) S[i][j] = rnd(S[i][j] + chunk_value(P[i][j]));
             }
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) P[i][j] = 0.0f;
-            ++chunk;
+            ++chunk;                     // the next chunk starts with first_step
         };
 
         const int nk = kend - kbeg;
@@ -339,10 +335,10 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             while (kk < kmax) {
                 const int seg = min(kmax - kk, crem);
                 if (seg == BK) {
-                    // A slab that starts a chunk begins with a product into a
-                    // zero partial sum, exact and already an FP16 value (at
-                    // most 6 significant bits, well inside the range): one
-                    // fma with 0 (which also turns -0 into +0) and no rounding.
+                    // Every chunk begins with a product into a zero partial
+                    // sum, exact and already an FP16 value (at most 6
+                    // significant bits, well inside the range): one fma with 0
+                    // (which also turns -0 into +0) and no rounding.
                     const bool fresh = crem == g.CL;
                     if (PF) {
                         float a0[TM], b0[TN], a1[TM], b1[TN];
@@ -365,10 +361,12 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                         }
                     }
                 } else {
+                    const bool fresh = crem == g.CL;
                     for (int q = kk; q < kk + seg; ++q) {
                         float a[TM], b[TN];
                         lds_read(a, b, buf, q);
-                        fma_step(a, b);
+                        if (q == kk && fresh) first_step(a, b);
+                        else fma_step(a, b);
                     }
                 }
                 kk += seg;
