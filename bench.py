@@ -50,8 +50,8 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 257.5 MB, weight-gradient 3072.8 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on: any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "021ebf78d0b7d6f5e4dcc6686fbeab8df461bf10c149135c6f2da7ccf3613412"
-EXACT_TRAFFIC_BYTES_PER_CALL = 1175.4e6
+TRAFFIC_SOURCES_SHA256 = "287d5dcb6a547a1153ba8fb9e0f17cfdb28028c6f37a7192afef5cdfca829047"
+EXACT_TRAFFIC_BYTES_PER_CALL = 1175.3e6
 
 
 def kernel_sources_sha256():
