@@ -158,6 +158,8 @@ double valu_ops_per_mac(int cfg) {
         case 2: return 4.9;     // 8 x 4
         case 1: return 5.1;     // 8 x 8, 2 waves per SIMD
         case 0: return 5.2;
+        case 7: return 4.3;     // 4 x 4 on 128 x 64 tiles, 8 waves per workgroup
+        case 8: return 4.3;     // 4 x 4 on 64 x 128 tiles, 8 waves per workgroup
         case 5: return 6.5;     // 2 x 2
         default: return 10.0;   // 1 x 1
     }

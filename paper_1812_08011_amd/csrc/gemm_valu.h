@@ -12,7 +12,7 @@ struct ValuShape {
     int NT;         // threads per workgroup
 };
 
-constexpr int kValuConfigs = 7;
+constexpr int kValuConfigs = 9;
 
 ValuShape valu_shape(int cfg);
 

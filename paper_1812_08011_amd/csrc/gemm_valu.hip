@@ -16,6 +16,8 @@ ValuShape valu_shape(int cfg) {
         case 3: return valu_impl::shape_of<3>();
         case 4: return valu_impl::shape_of<4>();
         case 5: return valu_impl::shape_of<5>();
+        case 7: return valu_impl::shape_of<7>();
+        case 8: return valu_impl::shape_of<8>();
         default: return valu_impl::shape_of<6>();
     }
 }

@@ -511,6 +511,8 @@ template <> struct ValuCfg<3> { static constexpr int TM = 4, TN = 8, LM = 16, LN
 template <> struct ValuCfg<4> { static constexpr int TM = 4, TN = 4, LM = 16, LN = 16, BK = 32, WPE = 4; static constexpr bool PF = true; };
 template <> struct ValuCfg<5> { static constexpr int TM = 2, TN = 2, LM = 16, LN = 16, BK = 32, WPE = 8; static constexpr bool PF = false; };
 template <> struct ValuCfg<6> { static constexpr int TM = 1, TN = 1, LM = 16, LN = 16, BK = 64, WPE = 8; static constexpr bool PF = false; };
+template <> struct ValuCfg<7> { static constexpr int TM = 4, TN = 4, LM = 32, LN = 16, BK = 32, WPE = 4; static constexpr bool PF = true; };
+template <> struct ValuCfg<8> { static constexpr int TM = 4, TN = 4, LM = 16, LN = 32, BK = 32, WPE = 4; static constexpr bool PF = true; };
 
 template <int C, bool TA, bool TB, bool FAST>
 const void* kernel_of() {
@@ -539,6 +541,8 @@ const void* kernel_table(int cfg, int fast) {
         case 4: return kernel_of<4, TA, TB, false>();
         case 5: return kernel_of<5, TA, TB, false>();
         case 6: return kernel_of<6, TA, TB, false>();
+        case 7: return kernel_of<7, TA, TB, false>();
+        case 8: return kernel_of<8, TA, TB, false>();
         default: return nullptr;
     }
 }

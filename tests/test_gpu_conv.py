@@ -48,11 +48,14 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("plan", ["auto", "shared"])
+@pytest.mark.parametrize("plan", ["auto", "shared", "tile4", "tile7", "tile7-shared"])
 def test_conv_fwd_and_wgrad_match_oracle(plan, monkeypatch):
-    if plan == "shared":
+    if plan.endswith("shared"):
         monkeypatch.setenv("FP8T_GEMM_SPLIT", "1")
         monkeypatch.setenv("FP8T_GEMM_WGS", "5")
+    if plan.startswith("tile"):
+        # the two register-tile shapes the lowered-input kernels are built for
+        monkeypatch.setenv("FP8T_VALU_TILE", plan[4])
     rng = np.random.default_rng(1010)
     for (N, H, W, C, KH, KW, pad, stride, Cout, CL) in CASES:
         geom = (N, H, W, C, KH, KW, pad, stride)

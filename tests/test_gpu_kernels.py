@@ -158,7 +158,7 @@ def _operands(rng, M, N, K, ta, tb, scale=1.0):
     return A, B
 
 
-VALU_TILES = ["auto", "0", "1", "2", "3", "4", "5", "6"]
+VALU_TILES = ["auto", "0", "1", "2", "3", "4", "5", "6", "7", "8"]
 
 
 @pytest.mark.parametrize("guard", ["1", "0"])
@@ -193,7 +193,7 @@ SPLIT_SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("tile", ["1", "2", "4", "5", "6"])
+@pytest.mark.parametrize("tile", ["1", "2", "4", "5", "6", "7", "8"])
 @pytest.mark.parametrize("wgs", ["1", "3", "7", "50"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (1, 0), (0, 1)])
 def test_chunk_gemm_exact_shared_tiles(tile, wgs, ta, tb, monkeypatch):
