@@ -46,12 +46,12 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # HBM traffic of the exact-mode chunk_gemm calls of one step, from two
 # rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) over this benchmark,
 # calibrated by the counters of a plain device copy of known size (fetch x2.0,
-# write x1.0); average calibrated bytes per call (forward 196.2 MB,
-# backward-data 257.5 MB, weight-gradient 3072.8 MB including the chunk sums
+# write x1.0); average calibrated bytes per call (forward 195.2 MB,
+# backward-data 294.5 MB, weight-gradient 2402.5 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on: any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "287d5dcb6a547a1153ba8fb9e0f17cfdb28028c6f37a7192afef5cdfca829047"
-EXACT_TRAFFIC_BYTES_PER_CALL = 1175.3e6
+TRAFFIC_SOURCES_SHA256 = "985aa7ceb6bd51d39469c67925533704659ba77d373c1427108614188aaba5fd"
+EXACT_TRAFFIC_BYTES_PER_CALL = 964.1e6
 
 
 def kernel_sources_sha256():
