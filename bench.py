@@ -49,9 +49,16 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # write x1.0); average calibrated bytes per call (forward 195.2 MB,
 # backward-data 294.5 MB, weight-gradient 2402.5 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
-# they were measured on: any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "985aa7ceb6bd51d39469c67925533704659ba77d373c1427108614188aaba5fd"
+# they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
+TRAFFIC_SOURCES_SHA256 = "6635dbf51bf9a1141971aa06788b281a49661fce97971b38243d4c2d107ad2c2"
 EXACT_TRAFFIC_BYTES_PER_CALL = 964.1e6
+
+
+# The sources that decide what an exact-mode chunk_gemm call runs: the VALU
+# kernel, its instantiations, the planner and fold pass, the shared device code.
+EXACT_KERNEL_SOURCES = ("chunk_gemm.hip", "fp8t_device.h", "fp8t_host.h", "gemm_plan.h",
+                        "gemm_valu.h", "gemm_valu.hip", "gemm_valu_impl.h", "gemm_valu_nn.hip",
+                        "gemm_valu_nt.hip", "gemm_valu_tn.hip", "gemm_valu_tt.hip")
 
 
 def kernel_sources_sha256():
@@ -59,7 +66,7 @@ def kernel_sources_sha256():
     d = os.path.join(ROOT, "paper_1812_08011_amd", "csrc")
     h = hashlib.sha256()
     for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".h")):
+        if f in EXACT_KERNEL_SOURCES:
             h.update(f.encode())
             with open(os.path.join(d, f), "rb") as fh:
                 h.update(fh.read())

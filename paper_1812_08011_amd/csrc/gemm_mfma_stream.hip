@@ -1,8 +1,8 @@
 // chunk_gemm fast mode on the matrix cores: the streamed 64 x 64 kernel.
 //
 // Same arithmetic as chunk_gemm_mfma (gemm_mfma.hip), for CL a multiple of
-// 64: each chunk of CL products is summed in FP32 by v_mfma_f32_32x32x16_bf8_bf8 (the FP8 codes
-// are OCP E5M2 = bf8), rounded to FP16 once, and added into the running sum
+// 64: each chunk of CL products is summed in FP32 by v_mfma_f32_32x32x64_f8f6f4 with both
+// operands bf8 (the FP8 codes are OCP E5M2 = bf8), rounded to FP16 once, and added into the running sum
 // in ascending chunk order with FP16 rounding after every add.  The design
 // differs in how the work reaches the matrix cores and the VALU:
 //   * the register budget allows 4 waves per SIMD (the VALU epilogue, 8
@@ -29,6 +29,7 @@ namespace fp8t {
 namespace {
 
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef int v8i __attribute__((ext_vector_type(8)));
 
 constexpr int kNT = 256;               // 4 waves, 2 x 2 blocks of 32 x 32
 constexpr int kB = 64;                 // tile rows = columns = slab k
@@ -161,9 +162,8 @@ struct Work {
     }
 };
 
-// Result register r of lane l (32x32x16): row 8 (r / 4) + 4 (l / 32) + r % 4,
-// column l % 32; operand bytes of lane l: row (or column) l % 32, k
-// 8 (l / 32) .. +7 of the 16-k step.
+// Result register r of lane l (32 x 32 blocks): row 8 (r / 4) + 4 (l / 32) + r % 4,
+// column l % 32; operand bytes of lane l: row (or column) l % 32.
 __device__ __forceinline__ int out_row(int l, int r) { return 8 * (r / 4) + 4 * (l / 32) + r % 4; }
 
 template <bool TA, bool TB>
@@ -179,7 +179,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
     const int lane = tid & 63, wave = tid >> 6;
     const int wy = wave >> 1, wx = wave & 1;
     const int arow = wy * 32 + (lane & 31), bcol = wx * 32 + (lane & 31);
-    const int kh = 8 * (lane >> 5);
+    const int kq = 32 * (lane >> 5);
     // with the guarded epilogue switched off every piece takes the safe one
     if (tid == 0) n_redo = g.guarded ? 0 : kRedoMax + 1;
 
@@ -244,24 +244,29 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
     };
 
     // The products of one slab (LDS buffer buf, k from ks) of item it.  CL is
-    // a multiple of 64, so a chunk ends only at a slab end: the four steps of
-    // a slab are one run of matrix-core instructions (past kend the operands
-    // are zero), and crem counts the k left in the current chunk.
+    // a multiple of 64, so a chunk ends only at a slab end: a slab is one
+    // 32 x 32 x 64 matrix-core instruction per wave (past kend the operands
+    // are zero), and crem counts the k left in the current chunk.  The
+    // instruction sums over all 64 k of its operands, so which lane half and
+    // byte holds which k only has to agree between A and B: lane half h holds
+    // k 32 h .. 32 h + 31 of both, in order.
     auto slab = [&](auto safe_tag, const Item& it, int buf, int ks, int& crem, int& chunk)
                     __attribute__((always_inline)) {
-        long a[4], b[4];
+        v8i a8, b8;
 #pragma unroll
-        for (int st = 0; st < 4; ++st) {
-            a[st] = *reinterpret_cast<const long*>(&As[buf][arow][16 * st + kh]);
-            b[st] = *reinterpret_cast<const long*>(&Bs[buf][bcol][16 * st + kh]);
+        for (int j = 0; j < 4; ++j) {
+            const long av = *reinterpret_cast<const long*>(&As[buf][arow][kq + 8 * j]);
+            const long bv = *reinterpret_cast<const long*>(&Bs[buf][bcol][kq + 8 * j]);
+            a8[2 * j] = (int)av;
+            a8[2 * j + 1] = (int)(av >> 32);
+            b8[2 * j] = (int)bv;
+            b8[2 * j + 1] = (int)(bv >> 32);
         }
+        // format selectors 1, 1: both operands bf8 (= the FP8 codes); no scaling
         if (crem == g.CL)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf8_bf8(a[0], b[0], zero, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, zero, 1, 1, 0, 0, 0, 0);
         else
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf8_bf8(a[0], b[0], acc, 0, 0, 0);
-#pragma unroll
-        for (int st = 1; st < 4; ++st)
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf8_bf8(a[st], b[st], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, acc, 1, 1, 0, 0, 0, 0);
         crem -= kB;
         if (crem == 0 || ks + kB >= it.kend) {
             chunk_end(safe_tag, it, it.m0, it.n0, chunk);
