@@ -84,12 +84,14 @@ __device__ __forceinline__ float dec_hi(uint32_t w) {        // code in bits 16.
     const uint32_t t = (((w >> 16) & 0x7FFFu) << 14) + (96u << 23);
     return __uint_as_float((w & 0x80000000u) | t);
 }
-// SR16 of a float in [2^-30, 2^31) in magnitude; r14 = the 16-bit uniform >> 2
-// (u < 4 D exactly when (u >> 2) < D for the 14 discarded bits D).
-__device__ __forceinline__ float sr16_normal(float x, uint32_t r14) {
-    const uint32_t u = __float_as_uint(x);
-    const uint32_t up = (u & 0x3FFFu) > r14 ? 0x4000u : 0u;
-    return __uint_as_float((u & 0xFFFFC000u) + up);
+// SR16 of a float in [2^-30, 2^31) in magnitude.  The magnitude goes up one
+// step (2^14 in the raw bits) exactly when the 14 discarded bits D exceed
+// r = u16 >> 2 (u16 < 4 D exactly when (u16 >> 2) < D), i.e. when D + (2^14 - 1
+// - r) carries into bit 14: so add c14 = 2^14 - 1 - r = (~u16 >> 2) & (2^14 - 1)
+// to the raw bits and clear the low 14 (the carry cannot reach the exponent's
+// top, the magnitude staying below 2^31).
+__device__ __forceinline__ float sr16_normal(float x, uint32_t c14) {
+    return __uint_as_float((__float_as_uint(x) + c14) & 0xFFFFC000u);
 }
 __device__ __forceinline__ uint32_t enc_normal(float v) {   // FP16 code
     const uint32_t u = __float_as_uint(v);
@@ -101,9 +103,11 @@ __device__ __forceinline__ bool update_pair_normal(const u32x4& rnd, uint32_t wp
                                                    uint32_t vp, const upd_params& p,
                                                    uint32_t& w_out, uint32_t& v_out,
                                                    float (&w1)[2]) {
-    const uint32_t r[6] = {__builtin_amdgcn_ubfe(rnd.x, 2, 14), __builtin_amdgcn_ubfe(rnd.x, 18, 14),
-                           __builtin_amdgcn_ubfe(rnd.y, 2, 14), __builtin_amdgcn_ubfe(rnd.y, 18, 14),
-                           __builtin_amdgcn_ubfe(rnd.z, 2, 14), __builtin_amdgcn_ubfe(rnd.z, 18, 14)};
+    // 2^14 - 1 - (u16 >> 2) of the six uniforms: the complemented halves' top 14 bits
+    const uint32_t nx = ~rnd.x, ny = ~rnd.y, nz = ~rnd.z;
+    const uint32_t r[6] = {__builtin_amdgcn_ubfe(nx, 2, 14), __builtin_amdgcn_ubfe(nx, 18, 14),
+                           __builtin_amdgcn_ubfe(ny, 2, 14), __builtin_amdgcn_ubfe(ny, 18, 14),
+                           __builtin_amdgcn_ubfe(nz, 2, 14), __builtin_amdgcn_ubfe(nz, 18, 14)};
     const float w[2] = {dec_lo(wp), dec_hi(wp)};
     const float g[2] = {dec_lo(gp), dec_hi(gp)};
     float lo = 0x1p31f, hi = 0.0f;
@@ -279,10 +283,11 @@ __device__ __forceinline__ bool adam_pair_normal(const u32x4& rnd, uint32_t wp, 
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
         // element e takes uniforms 4e .. 4e+3 = the halves of words 2e, 2e+1
-        const uint32_t r0 = __builtin_amdgcn_ubfe(words[2 * e], 2, 14);
-        const uint32_t r1 = __builtin_amdgcn_ubfe(words[2 * e], 18, 14);
-        const uint32_t r2 = __builtin_amdgcn_ubfe(words[2 * e + 1], 2, 14);
-        const uint32_t r3 = __builtin_amdgcn_ubfe(words[2 * e + 1], 18, 14);
+        // 2^14 - 1 - (u16 >> 2) of the four uniforms (see sr16_normal)
+        const uint32_t r0 = __builtin_amdgcn_ubfe(~words[2 * e], 2, 14);
+        const uint32_t r1 = __builtin_amdgcn_ubfe(~words[2 * e], 18, 14);
+        const uint32_t r2 = __builtin_amdgcn_ubfe(~words[2 * e + 1], 2, 14);
+        const uint32_t r3 = __builtin_amdgcn_ubfe(~words[2 * e + 1], 18, 14);
         const float w = e ? dec_hi(wp) : dec_lo(wp), g = e ? dec_hi(gp) : dec_lo(gp);
         const float m = e ? dec_hi(mp) : dec_lo(mp), v = e ? dec_hi(vp) : dec_lo(vp);
         const float x1 = __builtin_fmaf(p.weight_decay, w, g);
