@@ -110,34 +110,34 @@ __device__ __forceinline__ bool update_pair_normal(const u32x4& rnd, uint32_t wp
                            __builtin_amdgcn_ubfe(nz, 2, 14), __builtin_amdgcn_ubfe(nz, 18, 14)};
     const float w[2] = {dec_lo(wp), dec_hi(wp)};
     const float g[2] = {dec_lo(gp), dec_hi(gp)};
-    float lo = 0x1p31f, hi = 0.0f;
+    float lo[2], hi[2];
     uint32_t wc[2], vc[2] = {0u, 0u};
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
+        // the element's smallest and largest magnitude, in three-input
+        // min / max steps
         const float x1 = __builtin_fmaf(p.weight_decay, w[e], g[e]);
         float step = sr16_normal(x1, r[3 * e]);
-        lo = fminf(lo, fminf(fabsf(w[e]), fabsf(g[e])));
-        hi = fmaxf(hi, fmaxf(fabsf(w[e]), fabsf(g[e])));
-        lo = fminf(lo, fabsf(x1));
-        hi = fmaxf(hi, fabsf(x1));
+        lo[e] = fminf(fminf(fabsf(w[e]), fabsf(g[e])), fabsf(x1));
+        hi[e] = fmaxf(fmaxf(fabsf(w[e]), fabsf(g[e])), fabsf(x1));
         if (HAS_V) {
             const float v = e ? dec_hi(vp) : dec_lo(vp);
             const float x2 = __builtin_fmaf(p.momentum, v, step);
             step = sr16_normal(x2, r[3 * e + 1]);
             vc[e] = enc_normal(step);
-            lo = fminf(lo, fminf(fabsf(v), fabsf(x2)));
-            hi = fmaxf(hi, fmaxf(fabsf(v), fabsf(x2)));
+            lo[e] = fminf(fminf(lo[e], fabsf(v)), fabsf(x2));
+            hi[e] = fmaxf(fmaxf(hi[e], fabsf(v)), fabsf(x2));
         }
         const float x3 = __builtin_fmaf(-p.lr, step, w[e]);
         w1[e] = sr16_normal(x3, r[3 * e + 2]);
         wc[e] = enc_normal(w1[e]);
-        lo = fminf(lo, fabsf(x3));
-        hi = fmaxf(hi, fabsf(x3));
+        lo[e] = fminf(lo[e], fabsf(x3));
+        hi[e] = fmaxf(hi[e], fabsf(x3));
     }
     w_out = wc[0] | (wc[1] << 16);
     v_out = vc[0] | (vc[1] << 16);
     // NaN never arises from values in range; comparisons are false for it
-    return lo >= 0x1p-30f && hi < 0x1p31f;
+    return fminf(lo[0], lo[1]) >= 0x1p-30f && fmaxf(hi[0], hi[1]) < 0x1p31f;
 }
 
 // One thread updates PAIRS consecutive element pairs (PAIRS = 1, 2 or 4; the
