@@ -50,7 +50,7 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 294.5 MB, weight-gradient 2402.5 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "6635dbf51bf9a1141971aa06788b281a49661fce97971b38243d4c2d107ad2c2"
+TRAFFIC_SOURCES_SHA256 = "7bea62416d5ba590b1c3315a57ad4f4ea579e99fd444d16bd08d6a1f6a58d773"
 EXACT_TRAFFIC_BYTES_PER_CALL = 963.7e6
 
 

@@ -112,7 +112,8 @@ int fp16_quantize(const float* src, uint16_t* dst, int64_t n,
  * call takes the fastest plan that needs none; otherwise workspace_bytes must
  * be at least chunk_gemm_workspace_size(...) for the same arguments on the
  * same device.  Its contents on entry do not matter.
- * Errors: FP8T_EINVAL (negative size, CL < 1, flag not 0/1, a leading
+ * Errors: FP8T_EINVAL (negative size, M, N or K above 2^31 - 4097 -- the
+ * kernels index in 32 bits --, CL < 1, flag not 0/1, a leading
  * dimension too small, NULL pointer for a non-empty matrix, NULL workspace
  * with workspace_bytes > 0); FP8T_EWORKSPACE (0 < workspace_bytes < the
  * query); FP8T_EHIP.

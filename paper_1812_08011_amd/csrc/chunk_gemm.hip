@@ -131,12 +131,13 @@ __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, in
 // K = 0: every result is +0 (FP16 code 0, FP8 code of 0 * scale).
 __global__ void fill_empty(uint16_t* __restrict__ C, int64_t ldc, uint8_t* __restrict__ C8,
                            int64_t ldc8, float scale, int M, int N) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t total = (int64_t)M * N;
-    if (i >= total) return;
-    const int64_t r = i / N, c = i % N;
-    if (C) C[r * ldc + c] = 0;
-    if (C8) C8[r * ldc8 + c] = (uint8_t)f32_to_fp8(0.0f * scale);
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += step) {
+        const int64_t r = i / N, c = i % N;
+        if (C) C[r * ldc + c] = 0;
+        if (C8) C8[r * ldc8 + c] = (uint8_t)f32_to_fp8(0.0f * scale);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -320,7 +321,7 @@ bool gemm_args_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, i
     if ((ta != 0 && ta != 1) || (tb != 0 && tb != 1)) return false;
     if (mode != FP8T_EXACT && mode != FP8T_FAST) return false;
     // indices inside the kernels are 32-bit per dimension
-    if (M > INT32_MAX || N > INT32_MAX || K > INT32_MAX) return false;
+    if (M > kMaxGemmDim || N > kMaxGemmDim || K > kMaxGemmDim) return false;
     return true;
 }
 
@@ -365,7 +366,7 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     const int m = (int)M, n = (int)N, k = (int)K, cl = (int)(K > 0 ? CL : 1);
     if (K == 0) {
         const int64_t total = M * N;
-        hipLaunchKernelGGL(fill_empty, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+        hipLaunchKernelGGL(fill_empty, dim3(stride_blocks(total, 256)), dim3(256), 0,
                            stream, C, ldc, C8, ldc8, scale, m, n);
         return launch_status();
     }
@@ -460,7 +461,7 @@ ConvShape conv_shape(int64_t N, int64_t H, int64_t W, int64_t C, int64_t KH, int
     r.M = N * r.OH * r.OW;
     r.K = KH * KW * C;
     // every index of X, Xcol and the GEMM in 32 bits
-    if (r.M > INT32_MAX || r.K > INT32_MAX || N * H * W * C > ((int64_t)1 << 40)) return r;
+    if (r.M > kMaxGemmDim || r.K > kMaxGemmDim || N * H * W * C > ((int64_t)1 << 40)) return r;
     r.ok = true;
     return r;
 }
@@ -471,7 +472,7 @@ int conv_gemm_call(bool wgrad, const uint8_t* X, int64_t N, int64_t H, int64_t W
                    int64_t Cout, int64_t CL, uint16_t* Out, int64_t ldo, void* workspace,
                    size_t workspace_bytes, hipStream_t stream, bool query, size_t* need) {
     const ConvShape cs = conv_shape(N, H, W, C, KH, KW, pad, stride);
-    if (!cs.ok || Cout < 0 || CL < 1) return FP8T_EINVAL;
+    if (!cs.ok || Cout < 0 || Cout > kMaxGemmDim || CL < 1) return FP8T_EINVAL;
     // GEMM dimensions: fwd  Y (M x Cout) = Xcol (M x K) W (K x Cout);
     //                  wgrad dW (K x Cout) = Xcol^T (K x M) dY (M x Cout)
     const int64_t gM = wgrad ? cs.K : cs.M, gN = Cout, gK = wgrad ? cs.M : cs.K;
@@ -489,7 +490,7 @@ int conv_gemm_call(bool wgrad, const uint8_t* X, int64_t N, int64_t H, int64_t W
     if (workspace_bytes > 0 && !workspace) return FP8T_EINVAL;
     if (gK == 0) {
         const int64_t total = gM * gN;
-        hipLaunchKernelGGL(fill_empty, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+        hipLaunchKernelGGL(fill_empty, dim3(stride_blocks(total, 256)), dim3(256), 0,
                            stream, Out, ldo, (uint8_t*)nullptr, (int64_t)0, 1.0f, (int)gM,
                            (int)gN);
         return launch_status();

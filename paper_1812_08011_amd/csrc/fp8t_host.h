@@ -11,6 +11,18 @@
 
 namespace fp8t {
 
+// Largest M, N or K a GEMM entry point accepts: the kernels index rows,
+// columns and k in 32 bits and form tile and slab ends (up to 4096 past an
+// index) without overflow.
+constexpr int64_t kMaxGemmDim = INT32_MAX - 4096;
+
+// Blocks of a grid-stride launch over `total` items, `per_block` per block
+// and pass: enough to fill the chip, never beyond the grid's limit.
+inline unsigned stride_blocks(int64_t total, int per_block) {
+    const int64_t b = (total + per_block - 1) / per_block;
+    return (unsigned)(b < 65536 ? (b > 0 ? b : 1) : 65536);
+}
+
 inline bool aligned(const void* p, uintptr_t a) {
     return ((uintptr_t)p % a) == 0;
 }

@@ -497,9 +497,10 @@ __global__ __launch_bounds__(256) void chunk_fold_tile(TileArgs g, Plan p) {
 }
 
 __global__ void fill_zero16(uint16_t* __restrict__ C, int64_t ldc, int M, int N) {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)M * N) return;
-    C[(i / N) * ldc + i % N] = 0;
+    const int64_t total = (int64_t)M * N;
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += step)
+        C[(i / N) * ldc + i % N] = 0;
 }
 
 template <int FMT, bool SR>
@@ -564,7 +565,7 @@ bool tile_args_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL) {
     if (M < 0 || N < 0 || K < 0 || CL < 1) return false;
     if ((ta != 0 && ta != 1) || (tb != 0 && tb != 1)) return false;
     // 32-bit indices inside the kernel (k also runs one slab past K)
-    return M <= INT32_MAX && N <= INT32_MAX && K <= INT32_MAX - 2 * kBK;
+    return M <= kMaxGemmDim && N <= kMaxGemmDim && K <= kMaxGemmDim;
 }
 
 // Validation, K = 0, planning and launch shared by the two entry points.
@@ -582,7 +583,7 @@ int tile_call(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, const
     if (workspace_bytes > 0 && !workspace) return FP8T_EINVAL;
     if (K == 0) {
         const int64_t total = M * N;
-        hipLaunchKernelGGL(fill_zero16, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+        hipLaunchKernelGGL(fill_zero16, dim3(stride_blocks(total, 256)), dim3(256), 0,
                            stream, C, ldc, (int)M, (int)N);
         return launch_status();
     }

@@ -92,6 +92,8 @@ def test_chunk_gemm_rejects(lib):
     assert _gemm(lib, B=None) == E
     assert _gemm(lib, C=None) == E
     assert _gemm(lib, M=2 ** 31) == E                   # beyond 32-bit dimensions
+    assert _gemm(lib, N=2 ** 31 - 4096, ldb=2 ** 31, ldc=2 ** 31) == E  # no room for tile ends
+    assert _gemm(lib, K=2 ** 31 - 4096, lda=2 ** 31) == E
     assert _gemm(lib, M=0) == fp8t.OK                   # empty output: no-op
     assert _gemm(lib, N=0, C=None) == fp8t.OK
 
@@ -189,7 +191,8 @@ def test_conv_rejects(lib):
                                   a["ldy"], a["ws"], a["wsb"], None)
     for bad in (dict(N=-1), dict(H=0), dict(C=0), dict(KH=0), dict(stride=0), dict(pad=-1),
                 dict(KH=8), dict(Cout=-1), dict(CL=0), dict(X=None), dict(Wt=None),
-                dict(Y=None), dict(ldy=7), dict(ws=None, wsb=16)):
+                dict(Y=None), dict(ldy=7), dict(ws=None, wsb=16),
+                dict(Cout=2 ** 31 - 4096, ldy=2 ** 31)):
         assert fwd(**bad) == E, bad
     assert fwd(N=0) == fp8t.OK
     assert fwd(Cout=0) == fp8t.OK
