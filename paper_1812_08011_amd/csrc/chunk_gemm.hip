@@ -169,19 +169,23 @@ double valu_ops_per_mac(int cfg) {
 // Matrix-core fast mode, CU time of one output-chunk (the VALU epilogue
 // dominates; the matrix-core share grows with CL) and of the per-tile start
 // (pipeline fill, C stores), measured on the conv-stage GEMMs: 64 x 64 tiles
-// with 64-k slabs, 32 x 32 tiles with 128-k slabs, and the streamed 64 x 64
-// kernel (fitted to its forward and backward-data times).
+// with 64-k slabs, 32 x 32 tiles with 128-k slabs, the streamed 64 x 64
+// kernel (fitted to its forward and backward-data times) and the 64 x 64
+// kernel with chunks spread over 16 waves (fitted to all three).
 double mfma_cost_per_output_chunk(int cfg, int64_t CL) {
-    const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : 0.099e-9;
+    const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : cfg == 2 ? 0.099e-9 : 0.11e-9;
     return base * (0.6 + 0.4 * (double)CL / 64.0);
 }
-double mfma_cost_per_tile(int cfg) { return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : 0.77e-6; }
+double mfma_cost_per_tile(int cfg) {
+    return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.77e-6 : 0.85e-6;
+}
 
 enum Kind { VALU_EXACT = 0, VALU_FAST = 1, MFMA_FAST = 2 };
 
 struct Choice {
     int cfg = -1;
     const void* fn = nullptr;
+    const void* fn_aligned = nullptr;    // variant taken when mfma_kx_aligned(args)
     int NT = 0, BM = 0, BN = 0;
     Plan plan{};
     size_t ws_bytes = 0;
@@ -219,6 +223,7 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
             if (mf) {
                 const MfmaShape sh = mfma_shape(cfg);
                 if (CL % sh.kstep != 0) continue;
+                if (cfg == 3 && CL != 64) continue;     // one chunk per wave and step
                 fn = mfma_kernel(cfg, ta, tb);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
                 t_out = mfma_cost_per_output_chunk(cfg, CL);
@@ -248,8 +253,9 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 double est;
                 size_t ws = 0;
                 // the streamed kernel writes split tiles' chunk sums as scattered
-                // 2-byte stores: the other kernels are faster there
-                if (split && mf && cfg == 2) continue;
+                // 2-byte stores: the other kernels are faster there; the
+                // chunk-per-wave kernel has no shared tiles
+                if (split && mf && cfg >= 2) continue;
                 if (!split) {
                     const int64_t G = T < gmax ? T : gmax;
                     p.G = (int)G;
@@ -284,6 +290,7 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 if (best.cfg < 0 || est < best.est_s) {
                     best.cfg = cfg;
                     best.fn = fn;
+                    best.fn_aligned = mf && cfg == 3 ? mfma_kx_kernel_aligned(ta, tb) : nullptr;
                     best.NT = NT;
                     best.BM = BM;
                     best.BN = BN;
@@ -299,7 +306,8 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
 
 int launch_plan(const Choice& ch, GemmArgs g, hipStream_t stream) {
     void* args[] = {&g, const_cast<Plan*>(&ch.plan)};
-    if (hipLaunchKernel(ch.fn, dim3(ch.plan.G), dim3(ch.NT), args, 0, stream) != hipSuccess)
+    const void* fn = ch.fn_aligned && mfma_kx_aligned(g) ? ch.fn_aligned : ch.fn;
+    if (hipLaunchKernel(fn, dim3(ch.plan.G), dim3(ch.NT), args, 0, stream) != hipSuccess)
         return FP8T_EHIP;
     if (ch.plan.L > 0) {
         const int64_t shared = ch.plan.L / ch.plan.nch;

@@ -15,7 +15,7 @@ struct MfmaShape {
     int BK;         // k per LDS slab
 };
 
-constexpr int kMfmaConfigs = 3;
+constexpr int kMfmaConfigs = 4;
 
 MfmaShape mfma_shape(int cfg);
 
@@ -25,5 +25,13 @@ const void* mfma_kernel(int cfg, int ta, int tb);
 
 // The streamed 64 x 64 kernel (gemm_mfma_stream.hip), configuration 2.
 const void* mfma_stream_kernel(int ta, int tb);
+
+// 64 x 64 tiles with a step's four chunks spread over the workgroup's 16 waves
+// (gemm_mfma_kx.hip), configuration 3: CL = 64 only, whole tiles only.
+const void* mfma_kx_kernel(int ta, int tb);
+// Its variant for M and N multiples of 64, K a multiple of 256 and 16-byte
+// loads of both operands (mfma_kx_aligned): one load path, deeper prefetch.
+bool mfma_kx_aligned(const GemmArgs& g);
+const void* mfma_kx_kernel_aligned(int ta, int tb);
 
 }  // namespace fp8t

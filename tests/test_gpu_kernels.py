@@ -237,7 +237,7 @@ def test_chunk_gemm_workspace_contract():
         assert np.array_equal(host(C), Co)
 
 
-@pytest.mark.parametrize("mtile", ["auto", "0", "1", "2"])
+@pytest.mark.parametrize("mtile", ["auto", "0", "1", "2", "3"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
     """Fast mode against the fast oracle within the derived tolerance, for
@@ -282,6 +282,74 @@ def test_chunk_gemm_fast_shared_tiles(mtile, wgs, ta, tb, monkeypatch):
         monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
         Cs = host(gemm(Ad, Bd, M, N, K, CL, ta, tb, mode=fp8t.FAST))
         assert np.array_equal(Cw, Cs), (M, N, K, CL, np.argwhere(Cw != Cs)[:5])
+
+
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_chunk_gemm_fast_chunks_over_waves_same_bits(ta, tb, monkeypatch):
+    """The kernel that spreads a step's four chunks over the waves of a
+    64 x 64 tile (CL = 64) feeds the matrix cores the same bytes per chunk as
+    the streamed 64 x 64 kernel and adds the chunk sums in the same order, so
+    the two give the same bits: ragged M, N and K (steps with 1-3 chunks and
+    a short last chunk), padded leading dimensions and misaligned bases
+    (4-byte and byte-wise loads), both epilogues; and the fast oracle's
+    tolerance holds."""
+    rng = np.random.default_rng(590 + 2 * ta + tb)
+    # the last three are whole 64 x 64 tiles with K a multiple of 256 and
+    # 16-byte rows (the kernel's single-load-path variant); the last one has
+    # tiles that fail the overflow guard
+    cases = [(32, 32, 64, 0, 0), (33, 31, 65, 0, 0), (100, 70, 64 * 9 + 17, 0, 0),
+             (64, 96, 64 * 14, 0, 0), (70, 45, 64 * 23 + 40, 5, 1), (40, 72, 64 * 6, 3, 3),
+             (128, 64, 1024, 0, 0), (64, 128, 768, 0, 0), (128, 192, 512, 0, 0)]
+    for ci, (M, N, K, pad, off) in enumerate(cases):
+        A, B = _operands(rng, M, N, K, ta, tb)
+        if ci == len(cases) - 1:
+            (A.T if ta else A)[37, :] = 0x7B                     # 57344
+            (B if tb else B.T)[70, :] = np.where(rng.random(K) < 0.5, 0x7A, 0xFA)
+        # rows of lda (ldb) bytes starting off bytes into the allocation
+        lda, ldb = A.shape[1] + pad, B.shape[1] + pad
+        Ap = np.zeros((A.shape[0], lda), np.uint8)
+        Bp = np.zeros((B.shape[0], ldb), np.uint8)
+        Ap[:, :A.shape[1]] = A
+        Bp[:, :B.shape[1]] = B
+        Ad = dev(np.concatenate([np.zeros(off, np.uint8), Ap.ravel()]))[off:]
+        Bd = dev(np.concatenate([np.zeros(off, np.uint8), Bp.ravel()]))[off:]
+        got = {}
+        for mtile, wgs in (("2", "0"), ("3", "0"), ("3", "3")):
+            monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
+            monkeypatch.setenv("FP8T_GEMM_WGS", wgs)     # 3: several tiles per workgroup
+            for guard in ("1", "0"):
+                monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+                say(f"fast chunks over waves mtile={mtile} wgs={wgs} guard={guard} ta={ta} "
+                    f"tb={tb} {M}x{N}x{K} pad={pad} off={off}")
+                got[mtile + wgs, guard] = host(gemm(Ad, Bd, M, N, K, 64, ta, tb,
+                                                    mode=fp8t.FAST, lda=lda, ldb=ldb))
+        monkeypatch.delenv("FP8T_GEMM_WGS")
+        ref = got["20", "1"]
+        for key, C in got.items():
+            assert np.array_equal(C, ref), (key, M, N, K, np.argwhere(C != ref)[:5])
+        # the FP8 result in the same pass (with and without the FP16 one)
+        monkeypatch.setenv("FP8T_GEMM_GUARD", "1")
+        q8s = {}
+        for mtile in ("2", "3"):
+            monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
+            for with_c in (True, False):
+                C8 = torch.full((M, N + 3), 0xEE, dtype=torch.uint8, device=DEV)
+                C = torch.empty((M, N), dtype=torch.uint16, device=DEV) if with_c else None
+                ws_b = fp8t.chunk_gemm_fp8_workspace_size(ta, tb, M, N, K, 64, fp8t.FAST)
+                ws = torch.empty(max(ws_b, 1), dtype=torch.uint8, device=DEV)
+                fp8t.chunk_gemm_fp8(ta, tb, M, N, K, 64, Ad, lda, Bd, ldb, C, N, C8, N + 3,
+                                    0.5, fp8t.FAST, ws, ws_b)
+                q8s[mtile, with_c] = host(C8)
+                if with_c:
+                    assert np.array_equal(host(C), ref)
+        for key, Q in q8s.items():
+            assert np.array_equal(Q, q8s["2", True]), key
+        assert np.all(q8s["3", True][:, N:] == 0xEE)
+        assert np.array_equal(q8s["3", True][:, :N], oracle.fp8_quantize(ref, 0.5))
+        Co = oracle.chunk_gemm(A, B, 64, ta, tb, mode=oracle.FAST)
+        va = oracle.p8_value(A.T if ta else A)
+        vb = oracle.p8_value(B.T if tb else B)
+        check_fast(got["30", "1"], Co, abs_dot(va, vb), K, 64, f"fast kx {M}x{N}x{K}")
 
 
 def test_chunk_gemm_padded_leading_dims_and_misaligned_bases():
@@ -369,7 +437,7 @@ def test_chunk_gemm_guard_falls_back_per_piece(monkeypatch):
             assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
 
 
-@pytest.mark.parametrize("mtile", ["0", "1", "2"])
+@pytest.mark.parametrize("mtile", ["0", "1", "2", "3"])
 @pytest.mark.parametrize("wgs", ["0", "1"])
 def test_chunk_gemm_fast_guard_falls_back(mtile, wgs, monkeypatch):
     """Fast mode: pieces whose chunk sums reach 2^32 are recomputed on the
