@@ -170,14 +170,15 @@ double valu_ops_per_mac(int cfg) {
 // dominates; the matrix-core share grows with CL) and of the per-tile start
 // (pipeline fill, C stores), measured on the conv-stage GEMMs: 64 x 64 tiles
 // with 64-k slabs, 32 x 32 tiles with 128-k slabs, the streamed 64 x 64
-// kernel (fitted to its forward and backward-data times) and the 64 x 64
-// kernel with chunks spread over 16 waves (fitted to all three).
+// kernel and the 64 x 64 kernel with chunks spread over 16 waves (both
+// fitted to their forward and backward-data times; the latter predicts its
+// weight-gradient time within 5%).
 double mfma_cost_per_output_chunk(int cfg, int64_t CL) {
-    const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : cfg == 2 ? 0.099e-9 : 0.11e-9;
+    const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : cfg == 2 ? 0.0856e-9 : 0.0993e-9;
     return base * (0.6 + 0.4 * (double)CL / 64.0);
 }
 double mfma_cost_per_tile(int cfg) {
-    return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.77e-6 : 0.85e-6;
+    return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.67e-6 : 0.93e-6;
 }
 
 enum Kind { VALU_EXACT = 0, VALU_FAST = 1, MFMA_FAST = 2 };

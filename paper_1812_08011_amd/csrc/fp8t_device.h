@@ -121,6 +121,15 @@ __device__ __forceinline__ float rn16v(float x) {
     return c - d;
 }
 
+// max(m, |a|, |b|) in one instruction (the compiler splits the fmaxf form
+// into two or three).  For the GEMM guards: a NaN operand may or may not reach
+// the result, and either way the guarded and safe paths give the same bits.
+__device__ __forceinline__ float max3_abs(float m, float a, float b) {
+    float r;
+    asm("v_max3_f32 %0, %1, |%2|, |%3|" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+    return r;
+}
+
 // Plain float -> nearest FP16 code, ties to even; overflow -> Inf.
 __device__ __forceinline__ uint16_t f32_to_fp16_rn(float x) {
     uint32_t u = __float_as_uint(x);

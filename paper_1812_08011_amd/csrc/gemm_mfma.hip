@@ -239,7 +239,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                         } else {
                             const float pv = rn16v(acc[i][j][r]);
                             s = rn16v(S[i][j][r] + pv);
-                            vmax = fmaxf(vmax, fmaxf(fabsf(pv), fabsf(s)));
+                            vmax = max3_abs(vmax, pv, s);
                         }
                         S[i][j][r] = s;
                         acc[i][j][r] = 0.0f;

@@ -25,8 +25,9 @@
 //     aligned (AL) there is one load path, so the compiler waits for one set
 //     only; the workgroup streams on across its tiles;
 //   * the guarded epilogue (plain values, Veltkamp rounding, running max of
-//     |p| and |S|) runs in the stream; a tile in which a value reached 2^32
-//     (FP16 overflow) is remembered and recomputed after the stream with the
+//     |p| -- taken by the wave that rounds p -- and of |S|) runs in the
+//     stream; a tile in which a value reached 2^32 (FP16 overflow) is
+//     remembered and recomputed after the stream with the
 //     2^96-scaled epilogue (integer rounding on raw bits), which gives the
 //     same bits wherever the guarded one is valid.
 // Tiles are whole (no shared tiles, no workspace).
@@ -73,6 +74,12 @@ __device__ __forceinline__ void tr4(uint32_t d[4]) {
     d[3] = __builtin_amdgcn_perm(hi23, hi01, 0x07060302u);
 }
 
+// LDS byte offset, within an operand row, of the 8-byte k slot q: slots are
+// swizzled by bits 4-5 of the row, which spreads the 4-byte stores of the
+// transposed operands (16 rows 4 apart per half-wave) over all banks and
+// keeps each 32-byte half of a chunk where the matrix-core reads expect it.
+__device__ __forceinline__ int slot_off(int row, int q) { return 8 * (q ^ ((row >> 4) & 3)); }
+
 // One operand's share of a step (64 rows by 256 k): 16 bytes per thread.
 //   KC (element (r, k) at p[r ld + k]): row t / 16, k bytes 16 (t % 16) .. +15;
 //   otherwise (element (r, k) at p[k ld + r]): k rows 4 (t / 16) .. +3 by r
@@ -116,15 +123,16 @@ struct StepShare {
 
     __device__ __forceinline__ void store(uint8_t (*lds)[kPitch], int tid) {
         if (KC) {
-            uint8_t* d = &lds[tid >> 4][(tid & 15) * 16];
-            *reinterpret_cast<uint2*>(d) = make_uint2(w[0], w[1]);
-            *reinterpret_cast<uint2*>(d + 8) = make_uint2(w[2], w[3]);
+            const int r = tid >> 4, q = (tid & 15) * 2;
+            *reinterpret_cast<uint2*>(&lds[r][slot_off(r, q)]) = make_uint2(w[0], w[1]);
+            *reinterpret_cast<uint2*>(&lds[r][slot_off(r, q + 1)]) = make_uint2(w[2], w[3]);
         } else {
             uint32_t d[4] = {w[0], w[1], w[2], w[3]};
             tr4(d);
             const int kg = (tid >> 4) * 4, rg = (tid & 15) * 4;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) *reinterpret_cast<uint32_t*>(&lds[rg + i][kg]) = d[i];
+            for (int i = 0; i < 4; ++i)
+                *reinterpret_cast<uint32_t*>(&lds[rg + i][slot_off(rg + i, kg >> 3) + (kg & 4)]) = d[i];
         }
     }
 };
@@ -191,8 +199,8 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
         v8i a8, b8;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const long av = *reinterpret_cast<const long*>(&As[arow][kq + 8 * j]);
-            const long bv = *reinterpret_cast<const long*>(&Bs[bcol][kq + 8 * j]);
+            const long av = *reinterpret_cast<const long*>(&As[arow][slot_off(arow, kq / 8 + j)]);
+            const long bv = *reinterpret_cast<const long*>(&Bs[bcol][slot_off(bcol, kq / 8 + j)]);
             a8[2 * j] = (int)av;
             a8[2 * j + 1] = (int)(av >> 32);
             b8[2 * j] = (int)bv;
@@ -202,8 +210,17 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
         const v16f acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, zero, 1, 1, 0, 0,
                                                                         0, 0);
         float* dst = &Ps[wave][lane];
+        float pr[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dst[64 * r] = SAFE ? rn16s(acc[r] * 0x1p96f) : rn16v(acc[r]);
+        for (int r = 0; r < 16; ++r) {
+            pr[r] = SAFE ? rn16s(acc[r] * 0x1p96f) : rn16v(acc[r]);
+            dst[64 * r] = pr[r];
+        }
+        if (!SAFE) {
+            // the guard's largest |p| (its largest |S| is taken in chain)
+#pragma unroll
+            for (int r = 0; r < 16; r += 2) vmax = max3_abs(vmax, pr[r], pr[r + 1]);
+        }
     };
 
     // The running sums of the thread's 4 outputs over the step's chunks, in
@@ -224,14 +241,10 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
                 AL ? pvs[c] : *reinterpret_cast<const float4*>(&Ps[4 * cq + c][64 * sr + sl]);
             const float pp[4] = {pv.x, pv.y, pv.z, pv.w};
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                if (SAFE) {
-                    S[i] = rn16s(S[i] + pp[i]);
-                } else {
-                    const float t = rn16v(S[i] + pp[i]);
-                    vmax = fmaxf(vmax, fmaxf(fabsf(pp[i]), fabsf(t)));
-                    S[i] = t;
-                }
+            for (int i = 0; i < 4; ++i) S[i] = SAFE ? rn16s(S[i] + pp[i]) : rn16v(S[i] + pp[i]);
+            if (!SAFE) {
+                vmax = max3_abs(vmax, S[0], S[1]);
+                vmax = max3_abs(vmax, S[2], S[3]);
             }
         }
     };

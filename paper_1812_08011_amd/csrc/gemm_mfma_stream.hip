@@ -234,7 +234,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                 } else {
                     const float pv = rn16v(acc[r]);
                     s = rn16v(S[r] + pv);
-                    vmax = fmaxf(vmax, fmaxf(fabsf(pv), fabsf(s)));
+                    vmax = max3_abs(vmax, pv, s);
                 }
                 S[r] = s;
             }

@@ -42,7 +42,7 @@ def test_loss_gradient_and_relu_backward_values():
     d = oracle.fp16_quantize(np.float32([1.0, 2.0, -3.0, 0.1]))
     z = oracle.fp16_quantize(np.float32([0.5, -0.5, 0.0, 2.0]))
     got = oracle.p8_value(mlp.relu_backward_fp8(d, z))
-    assert list(got) == [1.0, 0.0, 0.0, float(oracle.p8_value(oracle.fp8_quantize(np.float32(0.1))))]
+    assert list(got) == [1.0, 0.0, 0.0, float(oracle.p8_value(oracle.fp8_quantize(np.float32([0.1])))[0])]
 
 
 def test_zero_rate_step_stores_backprop_gradients():
