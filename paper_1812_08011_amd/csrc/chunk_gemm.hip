@@ -90,35 +90,46 @@ __global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, in
         for (int v = 0; v < kFoldV; ++v)
             S[v] = rn16s(S[v] + fp16_to_f32s_fold((w[v / 2] >> (16 * (v % 2))) & 0xFFFFu));
     };
-    // two batches of kFoldU chunks: one in flight while the other is added
+    // two batches of kFoldU chunks: one in flight while the other is added.
+    // Every batch load is unconditional (chunk indices clamped to the last
+    // chunk, the extra values never added), so the compiler waits for the
+    // older batch only; a conditional load makes it wait for both.
+    const int last = p.nch - 1;
     auto load = [&](FoldVec (&q)[kFoldU], int c0) __attribute__((always_inline)) {
-        if (c0 + kFoldU <= p.nch) {
 #pragma unroll
-            for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)(c0 + u) * step];
-        } else {
-#pragma unroll
-            for (int u = 0; u < kFoldU; ++u)
-                if (c0 + u < p.nch) q[u] = src[(int64_t)(c0 + u) * step];
-        }
+        for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)min(c0 + u, last) * step];
     };
-    auto fold = [&](const FoldVec (&q)[kFoldU], int c0) __attribute__((always_inline)) {
-        if (c0 + kFoldU <= p.nch) {
+    auto fold_all = [&](const FoldVec (&q)[kFoldU]) __attribute__((always_inline)) {
 #pragma unroll
-            for (int u = 0; u < kFoldU; ++u) add(q[u]);
-        } else {
-#pragma unroll
-            for (int u = 0; u < kFoldU; ++u)
-                if (c0 + u < p.nch) add(q[u]);
-        }
+        for (int u = 0; u < kFoldU; ++u) add(q[u]);
     };
-    FoldVec q0[kFoldU], q1[kFoldU];
-    load(q0, a);
-    for (int c = a; c < p.nch; c += 2 * kFoldU) {
-        if (c + kFoldU < p.nch) load(q1, c + kFoldU);
-        fold(q0, c);
-        if (c + kFoldU >= p.nch) break;
-        if (c + 2 * kFoldU < p.nch) load(q0, c + 2 * kFoldU);
-        fold(q1, c + kFoldU);
+    auto fold_part = [&](const FoldVec (&q)[kFoldU], int n) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kFoldU; ++u)
+            if (u < n) add(q[u]);
+    };
+    if (a < p.nch) {
+        FoldVec q0[kFoldU], q1[kFoldU];
+        int c = a;
+        load(q0, c);
+        for (;;) {
+            // q0 holds chunks c ..
+            if (c + kFoldU > p.nch) {
+                fold_part(q0, p.nch - c);
+                break;
+            }
+            load(q1, c + kFoldU);
+            fold_all(q0);
+            c += kFoldU;
+            // q1 holds chunks c ..
+            if (c + kFoldU > p.nch) {
+                fold_part(q1, p.nch - c);
+                break;
+            }
+            load(q0, c + kFoldU);
+            fold_all(q1);
+            c += kFoldU;
+        }
     }
 #pragma unroll
     for (int v = 0; v < kFoldV; ++v) {
