@@ -46,12 +46,12 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # HBM traffic of the exact-mode chunk_gemm calls of one step, from two
 # rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) over this benchmark,
 # calibrated by the counters of a plain device copy of known size (fetch x2.0,
-# write x1.0); average calibrated bytes per call (forward 196.6 MB,
-# backward-data 294.5 MB, weight-gradient 2402.5 MB including the chunk sums
+# write x1.0); average calibrated bytes per call (forward 195.0 MB,
+# backward-data 294.4 MB, weight-gradient 2402.4 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "d527afafa72747fee29e7dc688eaafd9962f09802d50f1544db1608a82ec04e7"
-EXACT_TRAFFIC_BYTES_PER_CALL = 964.6e6
+TRAFFIC_SOURCES_SHA256 = "bd246e28d5834368b36295bf6d6edd6b7337afd266700602de80dc55bd36a07c"
+EXACT_TRAFFIC_BYTES_PER_CALL = 964.0e6
 
 
 # The sources that decide what an exact-mode chunk_gemm call runs: the VALU

@@ -56,12 +56,18 @@ __device__ __forceinline__ float fp16_to_f32s_fold(uint32_t c) {
 #ifndef FP8T_FOLD_U
 #define FP8T_FOLD_U 16
 #endif
-constexpr int kFoldV = FP8T_FOLD_V, kFoldU = FP8T_FOLD_U;
+#ifndef FP8T_FOLD_T
+#define FP8T_FOLD_T 64
+#endif
+// kFoldT threads per workgroup: one-wave workgroups spread evenly over the CUs
+// (the conv stage's weight-gradient fold is 2304 waves: 9 per CU, where
+// 256-thread workgroups left some CUs three and others two)
+constexpr int kFoldV = FP8T_FOLD_V, kFoldU = FP8T_FOLD_U, kFoldT = FP8T_FOLD_T;
 typedef std::conditional<kFoldV == 8, uint4, uint2>::type FoldVec;
 
-__global__ __launch_bounds__(256) void chunk_fold(GemmArgs g, Plan p, int BM, int BN) {
+__global__ __launch_bounds__(kFoldT) void chunk_fold(GemmArgs g, Plan p, int BM, int BN) {
     const int64_t per = (int64_t)BM * BN;
-    const int64_t idx = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kFoldV;
+    const int64_t idx = ((int64_t)blockIdx.x * kFoldT + threadIdx.x) * kFoldV;
     const int64_t lt = idx / per;
     if (lt * p.nch >= p.L) return;
     const int local = (int)(idx - lt * per);
@@ -324,7 +330,7 @@ int launch_plan(const Choice& ch, GemmArgs g, hipStream_t stream) {
     if (ch.plan.L > 0) {
         const int64_t shared = ch.plan.L / ch.plan.nch;
         const int64_t threads = shared * ch.BM * ch.BN / kFoldV;
-        hipLaunchKernelGGL(chunk_fold, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+        hipLaunchKernelGGL(chunk_fold, dim3((unsigned)((threads + kFoldT - 1) / kFoldT)), dim3(kFoldT), 0,
                            stream, g, ch.plan, ch.BM, ch.BN);
     }
     return launch_status();
