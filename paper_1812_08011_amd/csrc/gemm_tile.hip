@@ -451,7 +451,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_tile_kernel(TileArgs g, Plan p
 // SR, the same inter-chunk uniforms).  A thread takes 8 consecutive outputs
 // of a row: one 16-byte load of chunk sums (and one block of uniforms) per
 // chunk.
-constexpr int kFoldV = 8;
+constexpr int kFoldV = 8, kFoldTU = 8;
 
 template <bool SR>
 __global__ __launch_bounds__(256) void chunk_fold_tile(TileArgs g, Plan p) {
@@ -474,8 +474,8 @@ __global__ __launch_bounds__(256) void chunk_fold_tile(TileArgs g, Plan p) {
 #pragma unroll
     for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fp16_to_f32s(cp[v]) : 0.0f;
     const uint4* src = reinterpret_cast<const uint4*>(g.ws + lt * p.nch * per + local);
-    for (int c = a; c < p.nch; ++c) {
-        const uint4 q = src[(int64_t)c * (per / kFoldV)];
+    const int64_t step = per / kFoldV;
+    auto add = [&](const uint4& q, int c) __attribute__((always_inline)) {
         const uint32_t cw[4] = {q.x, q.y, q.z, q.w};
         uint32_t nw[4] = {0u, 0u, 0u, 0u};
         if (SR) {
@@ -490,6 +490,39 @@ __global__ __launch_bounds__(256) void chunk_fold_tile(TileArgs g, Plan p) {
             const float x = S[v] + fp16_to_f32s((cw[v / 2] >> (16 * (v % 2))) & 0xFFFFu);
             S[v] = SR ? sr16s(x, sr_addend(nw[v / 2], v % 2)) : rn16s(x);
         }
+    };
+    // Batches of kFoldTU chunk loads, the next batch in flight while one is
+    // added; every batch load is unconditional (indices clamped to the last
+    // chunk, the extra values never added) so the compiler waits for the
+    // older batch only.
+    const int last = p.nch - 1;
+    auto load = [&](uint4 (&q)[kFoldTU], int c0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kFoldTU; ++u) q[u] = src[(int64_t)min(c0 + u, last) * step];
+    };
+    auto fold = [&](const uint4 (&q)[kFoldTU], int c0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kFoldTU; ++u)
+            if (c0 + u < p.nch) add(q[u], c0 + u);
+    };
+    uint4 q0[kFoldTU], q1[kFoldTU];
+    int c = a;
+    load(q0, c);
+    for (;;) {
+        if (c + kFoldTU >= p.nch) {
+            fold(q0, c);
+            break;
+        }
+        load(q1, c + kFoldTU);
+        fold(q0, c);
+        c += kFoldTU;
+        if (c + kFoldTU >= p.nch) {
+            fold(q1, c);
+            break;
+        }
+        load(q0, c + kFoldTU);
+        fold(q1, c);
+        c += kFoldTU;
     }
 #pragma unroll
     for (int v = 0; v < kFoldV; ++v)
