@@ -132,7 +132,8 @@ def test_all_fp8_products_are_exact_in_fp16():
     a = np.repeat(np.arange(256, dtype=np.uint8), 256)
     b = np.tile(np.arange(256, dtype=np.uint8), 256)
     va, vb = oracle.p8_value(a), oracle.p8_value(b)
-    prod = va * vb                      # exact in float64
+    with np.errstate(invalid="ignore"):  # Inf x 0 -> NaN among the special codes
+        prod = va * vb                  # exact in float64
     codes = oracle.mul8(a, b)
     got = oracle.p16_value(codes)
     fin = np.isfinite(prod)
