@@ -176,12 +176,15 @@ size_t chunk_gemm_fp8_workspace_size(int trans_a, int trans_b, int64_t M,
  * is sr_weight_update's stochastic rounding into FP16 (Eq. (1), k = 9 of
  * k' = 23 bits, 16-bit uniform u: the magnitude is rounded up iff
  * u < 2^16 x the discarded fraction of a step).  The uniforms come from
- * Philox4x32-10 with key = (seed low, seed high), 16-bit halves of each word,
- * low half first: the addition of product k into output (i, j) uses uniform
- * k mod 8 of the block with counter (i, j, k / 8, 2 * offset), the addition
- * of chunk c into the running sum the low half of word 0 of the block with
- * counter (i, j, c, 2 * offset + 1).  The result is a pure function of the
- * inputs, seed and offset (bit-exact, independent of the device and plan).
+ * Philox4x32-10 with key = (seed low, seed high) and eight 16-bit uniforms
+ * per block (the halves of its four words, low half first: uniform q is
+ * half q mod 2 of word q / 2).  The addition of product k into output (i, j)
+ * uses uniform 4 (k mod 2) + (j mod 4) of the block with counter
+ * (i, j / 4, k / 2, 2 * offset); the addition of chunk c into the running sum
+ * of output (i, j) uses uniform j mod 8 of the block with counter
+ * (i, j / 8, c, 2 * offset + 1) (integer division; counter words in that
+ * order).  The result is a pure function of the inputs, seed and offset
+ * (bit-exact, independent of the device and plan).
  *
  * Layouts, CL, C and the workspace contract are those of chunk_gemm (with
  * chunk_gemm_sr_workspace_size as the query).  offset < 2^31.
@@ -259,7 +262,7 @@ int sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v, uint8_t* w8,
                      uint64_t seed, uint64_t offset, hipStream_t stream);
 
 /*
- * adam_update -- one ADAM step (Kingma & Ba; Sec. 4 trains with ADAM using
+ * adam_update -- one ADAM step (Kingma & Ba; Sec. 3 also trains with ADAM using
  * FP8 GEMMs and FP16 weight updates) with every AXPY stochastically rounded
  * into FP16 as in sr_weight_update, keeping FP16 master weights and moment
  * buffers and writing the FP8 weight copy.

@@ -157,6 +157,74 @@ int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
     return ORC_OK;
 }
 
+/* ---- the results the fast mode may give -----------------------------------
+ * The fast mode sums a chunk's products in FP32 in an order the matrix cores
+ * choose, so it has no single bit-exact result.  What it may give is bounded
+ * from the definition: the products are exact in FP32, and any FP32 sum of n
+ * terms with every addition rounded to nearest differs from the exact sum s
+ * by at most (n-1) u / (1 - (n-1) u) * sum|p|, u = 2^-24 (Higham, recursive
+ * summation in any order).  The bound taken here is looser,
+ * e = n u' / (1 - n u') * sum|p| with u' = 2^-22, so that it also holds for
+ * a matrix core that rounds towards zero, or aligns all addends to the
+ * largest exponent and truncates them to FP32's width before adding.
+ * Rounding to P16 and P16 addition are monotone, so the chunk's rounded sum
+ * lies between RN16(s - e) and RN16(s + e), and the
+ * running sum between the two chains
+ *     S_lo = RN16(S_lo + RN16(s_c - e_c)),  S_hi = RN16(S_hi + RN16(s_c + e_c))
+ * taken over the chunks in order (both from +0).  e_c is rounded up to the
+ * 2^-39 grid.  With e_c = 0 both chains are the fast oracle above.  A chunk
+ * whose exact sum is Inf or NaN gives the same value on both chains. */
+static void chunk_dot_fast_bounds(int trans_a, int trans_b, int64_t K, int64_t CL,
+                                  const uint8_t* A, int64_t lda, const uint8_t* B,
+                                  int64_t ldb, int64_t i, int64_t j,
+                                  uint16_t* lo, uint16_t* hi) {
+    xnum Slo = xn_zero(0), Shi = xn_zero(0);
+    for (int64_t c0 = 0; c0 < K; c0 += CL) {
+        int64_t c1 = (K - c0 < CL) ? K : c0 + CL;
+        xnum sum = xn_zero(0);
+        u128 absum = 0;
+        for (int64_t k = c0; k < c1; k++) {
+            xnum p = xn_mul_p8(op_a(trans_a, A, lda, i, k), op_b(trans_b, B, ldb, k, j));
+            sum = xn_add(sum, p);
+            if (p.cls == XN_FIN) absum += p.mag;
+        }
+        xnum Plo = sum, Phi = sum;
+        if (sum.cls == XN_FIN) {
+            const u128 n = (u128)(c1 - c0);
+            const u128 den = ((u128)1 << 22) - n;              /* 2^22 (1 - n u') */
+            const u128 e = (absum * n + den - 1) / den;        /* rounded up */
+            xnum d = {XN_FIN, 1, e};
+            Plo = xn_add(sum, d);
+            d.sign = 0;
+            Phi = xn_add(sum, d);
+        }
+        Slo = xn_from_p16(xn_round_p16(xn_add(Slo, xn_from_p16(xn_round_p16(Plo)))));
+        Shi = xn_from_p16(xn_round_p16(xn_add(Shi, xn_from_p16(xn_round_p16(Phi)))));
+    }
+    *lo = xn_round_p16(Slo);
+    *hi = xn_round_p16(Shi);
+}
+
+int cpu_chunk_gemm_fast_bounds_points(int trans_a, int trans_b, int64_t M, int64_t N,
+                                      int64_t K, int64_t CL, const uint8_t* A,
+                                      int64_t lda, const uint8_t* B, int64_t ldb,
+                                      const int64_t* rows, const int64_t* cols,
+                                      int64_t npts, uint16_t* lo, uint16_t* hi) {
+    if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, ORC_FAST))
+        return ORC_EINVAL;
+    if (CL > ((int64_t)1 << 21) && K > ((int64_t)1 << 21))
+        return ORC_EINVAL;                             /* keeps n u' <= 1/2 */
+    if (npts < 0 || (npts > 0 && (!rows || !cols || !lo || !hi))) return ORC_EINVAL;
+    for (int64_t p = 0; p < npts; p++)
+        if (rows[p] < 0 || rows[p] >= M || cols[p] < 0 || cols[p] >= N)
+            return ORC_EINVAL;
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t p = 0; p < npts; p++)
+        chunk_dot_fast_bounds(trans_a, trans_b, K, CL, A, lda, B, ldb, rows[p], cols[p],
+                              &lo[p], &hi[p]);
+    return ORC_OK;
+}
+
 /* ---- chunk-based accumulation with stochastic rounding -------------------
  * Sec. 2.3 names two rounding modes after P16 additions -- nearest and
  * stochastic -- and Fig. 3(b) compares them on long accumulations.  This is
@@ -373,7 +441,7 @@ int cpu_sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v,
 }
 
 /* ---- ADAM weight update in P16 with stochastic rounding -------------------
- * Sec. 4 also trains with the ADAM optimizer (Kingma & Ba) using FP8 GEMMs
+ * Sec. 3 also trains with the ADAM optimizer (Kingma & Ba) using FP8 GEMMs
  * and FP16 weight updates.  Read here as the SGD update above with ADAM's
  * moment estimates: every AXPY is formed in FP32 and stochastically rounded
  * into P16 (Eq. (1)), the moments are P16 buffers like the momentum buffer.

@@ -66,6 +66,16 @@ int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
                           const int64_t* rows, const int64_t* cols,
                           int64_t npts, uint16_t* out);
 
+/* Bounds on what the fast mode may give at the outputs (rows[p], cols[p]):
+ * every chunk's FP32 sum of n products, in any order, within
+ * n 2^-22 / (1 - n 2^-22) sum|p| of the exact one; lo[p] and hi[p] are the
+ * two monotone chains of ops.c.  Requires min(CL, K) <= 2^21. */
+int cpu_chunk_gemm_fast_bounds_points(int trans_a, int trans_b, int64_t M, int64_t N,
+                                      int64_t K, int64_t CL, const uint8_t* A,
+                                      int64_t lda, const uint8_t* B, int64_t ldb,
+                                      const int64_t* rows, const int64_t* cols,
+                                      int64_t npts, uint16_t* lo, uint16_t* hi);
+
 /* chunk_gemm with stochastic instead of nearest rounding after every P16
  * addition (Sec. 2.3, Fig. 3(b)); random bits keyed by (seed, i, j, k) as
  * described in ops.c.  Requires M, N <= 2^32, K / 2 < 2^32, offset < 2^31. */
@@ -93,7 +103,7 @@ int cpu_sr_weight_update(uint16_t* w, const uint16_t* g, uint16_t* v,
                          uint8_t* w8, int64_t n, float lr, float momentum,
                          float weight_decay, uint64_t seed, uint64_t offset);
 
-/* ADAM step in P16 with stochastic rounding (Sec. 4, Kingma & Ba), defined
+/* ADAM step in P16 with stochastic rounding (Sec. 3, Kingma & Ba), defined
  * in ops.c; m and v are the P16 moment buffers, updated in place; t >= 1 is
  * the step number.  orc_adam_step_size is its bias-corrected step size. */
 int cpu_adam_update(uint16_t* w, const uint16_t* g, uint16_t* m, uint16_t* v,

@@ -8,7 +8,11 @@
 // * chunk_gemm_valu (gemm_valu_impl.h) -- the exact mode, and the fast mode
 //   for chunk lengths the matrix cores cannot split;
 // * chunk_gemm_mfma (gemm_mfma.hip) -- the fast mode for CL a multiple of the
-//   MFMA instruction's K (16).
+//   MFMA instruction's K (16);
+// * chunk_gemm_mfma_stream (gemm_mfma_stream.hip) -- the fast mode for CL a
+//   multiple of 64, whole tiles streamed slab after slab;
+// * chunk_gemm_mfma_kx (gemm_mfma_kx.hip) -- the fast mode for CL = 64 on
+//   GEMMs with few outputs and a long K, a step's chunks spread over waves.
 #include <type_traits>
 
 #include "fp8t_device.h"

@@ -4,9 +4,8 @@
 // weights (Sec. 3).
 //
 // An element pair takes exactly one Philox4x32-10 block of random bits
-// (8 x 16-bit uniforms, 6 used); a thread handles 4 consecutive pairs.  The
-// kernel streams
-// 11 bytes per parameter (read w, g, v; write w, v, w8): at full size it is
+// (8 x 16-bit uniforms, 6 used); a thread handles one pair.  The kernel
+// streams 11 bytes per parameter (read w, g, v; write w, v, w8): at full size it is
 // HBM-bound, with Philox's 32-bit multiplies as the largest ALU cost.
 #include <cmath>
 

@@ -153,3 +153,23 @@ def brute_rn16(v):
 
 def to_fraction16(code):
     return p16_fraction(int(code))
+
+
+def p16_values(codes):
+    """Vectorised decode of FP16 (1,6,9) codes from the bit fields (float64;
+    Inf and NaN for exponent field 63)."""
+    c = np.asarray(codes, dtype=np.uint16).astype(np.int64)
+    e, m = (c >> 9) & 63, c & 511
+    mag = np.where(e == 0, m * 2.0 ** -39, (512 + m) * np.exp2(np.maximum(e, 1) - 40.0))
+    mag = np.where(e == 63, np.where(m == 0, np.inf, np.nan), mag)
+    return np.where(c & 0x8000, -mag, mag)
+
+
+def within_fast_bounds(C, lo, hi):
+    """Per output: is the FP16 code C between the codes lo and hi in value
+    (the fast mode's admissible results)?  NaN bounds admit only NaN."""
+    v, a, b = p16_values(C), p16_values(lo), p16_values(hi)
+    nan_b = np.isnan(a) | np.isnan(b)
+    with np.errstate(invalid="ignore"):
+        inside = (a <= v) & (v <= b)
+    return np.where(nan_b, np.isnan(v), inside)

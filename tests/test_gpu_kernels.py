@@ -12,6 +12,7 @@ import torch
 import oracle
 import paper_1812_08011_amd as fp8t
 from tests.gpu_util import DEV, dev, gemm, host, q8, q16, say
+from tests.helpers import within_fast_bounds
 
 pytestmark = pytest.mark.gpu
 
@@ -43,19 +44,34 @@ def abs_dot(A_vals, B_vals):
     return np.abs(A_vals) @ np.abs(B_vals)
 
 
-def check_fast(Cg, Co, absum, K, CL, what):
-    vg, vo = oracle.p16_value(Cg), oracle.p16_value(Co)
-    tol = fast_tolerance(absum, K, CL)
-    both_nan = np.isnan(vg) & np.isnan(vo)
-    same_inf = np.isinf(vg) & (vg == vo)
-    fin = ~(both_nan | same_inf)
-    assert np.all(np.isfinite(vg[fin])), what
-    diff = np.abs(vg[fin] - vo[fin])
-    bad = diff > tol[fin] + 1e-300
-    assert not bad.any(), (what, diff[bad][:5], tol[fin][bad][:5])
-    same = float(np.mean(Cg == Co))
-    say(f"{what}: fast vs fast-oracle bit-identical fraction {same:.4f}")
-    return same
+def check_fast(Cg, A, B, CL, ta, tb, what, *, rows=None, cols=None, Co=None, absum=None,
+               K=None):
+    """Fast-mode results against the oracle's bounds: every output must lie
+    between the two monotone FP16 chains built from each chunk's exact sum
+    minus and plus the float32 summation bound (any order).  Where the bounds
+    coincide the output is forced to the fast oracle's bits.  The looser
+    tolerance in units of sum|p| (`fast_tolerance`) is checked as well."""
+    lo, hi = oracle.chunk_gemm_fast_bounds(A, B, CL, ta, tb, rows, cols)
+    ok = within_fast_bounds(Cg, lo, hi)
+    bad = np.flatnonzero(~ok.ravel())
+    assert bad.size == 0, (what, bad[:5], Cg.ravel()[bad[:5]], lo.ravel()[bad[:5]],
+                           hi.ravel()[bad[:5]])
+    single = float(np.mean(lo == hi))
+    msg = f"{what}: inside the fast-mode bounds; single-valued bounds {single:.4f}"
+    if Co is not None:
+        assert within_fast_bounds(Co, lo, hi).all()
+        msg += f", bit-identical to the fast oracle {float(np.mean(Cg == Co)):.4f}"
+    say(msg)
+    if absum is not None:
+        vg, vo = oracle.p16_value(Cg), oracle.p16_value(Co)
+        tol = fast_tolerance(absum, K, CL)
+        both_nan = np.isnan(vg) & np.isnan(vo)
+        same_inf = np.isinf(vg) & (vg == vo)
+        fin = ~(both_nan | same_inf)
+        assert np.all(np.isfinite(vg[fin])), what
+        diff = np.abs(vg[fin] - vo[fin])
+        assert not (diff > tol[fin] + 1e-300).any(), what
+    return single
 
 
 # ---- quantization -------------------------------------------------------------
@@ -165,7 +181,7 @@ VALU_TILES = ["auto", "0", "1", "2", "3", "4", "5", "6", "7", "8"]
 @pytest.mark.parametrize("tile", VALU_TILES)
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_chunk_gemm_exact_matches_oracle(tile, ta, tb, guard, monkeypatch):
-    """Both paths of the exact kernel (guarded: scaled by 2^64 with Veltkamp
+    """Both paths of the exact kernel (guarded: plain values with Veltkamp
     rounding; safe: scaled by 2^96 with integer rounding) on every tile."""
     if tile != "auto":
         monkeypatch.setenv("FP8T_VALU_TILE", tile)
@@ -258,7 +274,8 @@ def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
         Co = oracle.chunk_gemm(A, B, CL, ta, tb, mode=oracle.FAST)
         va = oracle.p8_value(A.T if ta else A)
         vb = oracle.p8_value(B.T if tb else B)
-        check_fast(Cg, Co, abs_dot(va, vb), K, CL, f"fast {M}x{N}x{K} CL={CL}")
+        check_fast(Cg, A, B, CL, ta, tb, f"fast {M}x{N}x{K} CL={CL}", Co=Co,
+                   absum=abs_dot(va, vb), K=K)
         if CL == 1:
             assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, ta, tb))
 
@@ -349,7 +366,8 @@ def test_chunk_gemm_fast_chunks_over_waves_same_bits(ta, tb, monkeypatch):
         Co = oracle.chunk_gemm(A, B, 64, ta, tb, mode=oracle.FAST)
         va = oracle.p8_value(A.T if ta else A)
         vb = oracle.p8_value(B.T if tb else B)
-        check_fast(got["30", "1"], Co, abs_dot(va, vb), K, 64, f"fast kx {M}x{N}x{K}")
+        check_fast(got["30", "1"], A, B, 64, ta, tb, f"fast kx {M}x{N}x{K}", Co=Co,
+                   absum=abs_dot(va, vb), K=K)
 
 
 def test_chunk_gemm_padded_leading_dims_and_misaligned_bases():
@@ -376,9 +394,9 @@ def test_chunk_gemm_padded_leading_dims_and_misaligned_bases():
                 if mode == fp8t.EXACT:
                     assert np.array_equal(Ch[:, :N], Co)
                 else:
-                    check_fast(Ch[:, :N], Co, abs_dot(oracle.p8_value(A.T if ta else A),
-                                                      oracle.p8_value(B.T if tb else B)),
-                               K, CL, "padded fast")
+                    check_fast(Ch[:, :N], A, B, CL, ta, tb, "padded fast", Co=Co,
+                               absum=abs_dot(oracle.p8_value(A.T if ta else A),
+                                             oracle.p8_value(B.T if tb else B)), K=K)
 
 
 def test_chunk_gemm_degenerate():
@@ -433,6 +451,31 @@ def test_chunk_gemm_guard_falls_back_per_piece(monkeypatch):
             monkeypatch.setenv("FP8T_GEMM_SPLIT", split)
             monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
             say(f"guard fallback split={split} wgs={wgs}")
+            Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
+            assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
+
+
+@pytest.mark.parametrize("bmax", [0x44, 0x45])
+def test_chunk_gemm_guard_threshold(bmax, monkeypatch):
+    """All-positive operands with 9 K max|a| max|b| just below 2^31
+    (max|b| = 4: 2.114e9, the guarded path) and just above (max|b| = 5:
+    2.642e9, the safe path), every tile holding the maxima; both give the
+    oracle's bits, whole-tile and shared-tile plans alike."""
+    rng = np.random.default_rng(571)
+    M, N, K, CL = 192, 200, 1024, 64
+    A = rng.integers(0, 0x7B, (M, K)).astype(np.uint8)        # positive, < 57344
+    A[:, ::97] = 0x7B                                         # 57344 in every row
+    B = rng.integers(0, bmax, (K, N)).astype(np.uint8)
+    B[0, :] = bmax                                            # 4.0 or 5.0 in every column
+    bound = 9 * K * 57344 * float(oracle.p8_value(np.uint8(bmax)))
+    assert (bound < 2 ** 31) == (bmax == 0x44)
+    Co = oracle.chunk_gemm(A, B, CL)
+    for split, wgs in (("0", "0"), ("1", "7")):
+        for guard in ("1", "0"):
+            monkeypatch.setenv("FP8T_GEMM_SPLIT", split)
+            monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
+            monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+            say(f"guard threshold bmax={bmax:#x} split={split} wgs={wgs} guard={guard}")
             Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
             assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
 

@@ -55,7 +55,8 @@ def check_gemm_points(Ad, Bd, Ao, Bo, M, N, K, CL, ta, tb, npts, seed, what):
             assert np.array_equal(got, ref), (what, np.flatnonzero(got != ref)[:5])
         else:
             absum = np.einsum("pk,kp->p", np.abs(va_rows), np.abs(vb_cols))
-            check_fast(got, ref, absum, K, CL, f"{what} fast")
+            check_fast(got, Ao, Bo, CL, ta, tb, f"{what} fast", rows=r, cols=c, Co=ref,
+                       absum=absum, K=K)
 
 
 def test_small_workload_full():
@@ -69,8 +70,8 @@ def test_small_workload_full():
         if mode == fp8t.EXACT:
             assert np.array_equal(Cg, Co)
         else:
-            check_fast(Cg, Co, abs_dot(oracle.p8_value(Ao), oracle.p8_value(Bo)), 1024, 64,
-                       "small fast")
+            check_fast(Cg, Ao, Bo, 64, 0, 0, "small fast", Co=Co,
+                       absum=abs_dot(oracle.p8_value(Ao), oracle.p8_value(Bo)), K=1024)
     u = workloads.small_update()
     w16g, g16g = q16(dev(u["w"])), q16(dev(u["g"]))
     w16o, g16o = oracle.fp16_quantize(u["w"]), oracle.fp16_quantize(u["g"])

@@ -1,4 +1,4 @@
-"""Pins for the oracle's ADAM update in P16 with stochastic rounding (Sec. 4:
+"""Pins for the oracle's ADAM update in P16 with stochastic rounding (Sec. 3:
 ADAM with FP8 GEMMs and FP16 weight updates; Kingma & Ba's algorithm with the
 AXPYs of Sec. 2.2 rounded by Eq. (1)).
 

@@ -145,3 +145,28 @@ def test_sr_argument_checks():
     with pytest.raises(ValueError):
         oracle.chunk_gemm_sr(A, B, 4, seed=1, offset=2 ** 31)
     assert np.all(oracle.chunk_gemm_sr(A[:, :0], B[:0], 4, seed=1) == 0)
+
+
+def _header_text():
+    import os
+    import re
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "include", "fp8train.h")
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"\n\s*\*\s?", " ", text)          # join comment lines
+    return re.sub(r"\s+", " ", text)
+
+
+def test_header_documents_the_keying_tested_above():
+    """The public header states the random-bit keying that the independent
+    formulation above recomputes, so a caller reproducing a call from the
+    header gets the oracle's bits."""
+    doc = _header_text()
+    seg = doc[doc.index("chunk_gemm_sr -- "):doc.index("int chunk_gemm_sr(")]
+    for phrase in ("key = (seed low, seed high)",
+                   "low half first: uniform q is half q mod 2 of word q / 2",
+                   "uniform 4 (k mod 2) + (j mod 4) of the block with counter "
+                   "(i, j / 4, k / 2, 2 * offset)",
+                   "uniform j mod 8 of the block with counter (i, j / 8, c, 2 * offset + 1)"):
+        assert phrase in seg, phrase

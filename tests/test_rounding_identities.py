@@ -19,10 +19,11 @@ def veltkamp10(x):
 
 def test_veltkamp_split_is_round_to_nearest_even_on_whole_binades():
     """Exhaustive over every significand of binades spanning the exact GEMM's
-    guarded domain (values scaled by 2^64: 2^25 .. 2^96), both signs; ties
-    (frequent for sums of FP8 products) must go to even."""
+    guarded domain (unscaled FP16 values: normal from 2^-30 up to the 2^31
+    bound of the guard), both signs; ties (frequent for sums of FP8 products)
+    must go to even."""
     m = np.arange(1 << 23, dtype=np.uint32)
-    for e in (127 + 25, 127 + 40, 127 + 64, 127 + 95):
+    for e in (127 - 30, 127 - 1, 127, 127 + 30):
         for sign in (0, 1):
             u = (np.uint32(sign) << np.uint32(31)) | (np.uint32(e) << np.uint32(23)) | m
             x = u.view(np.float32)
@@ -31,9 +32,9 @@ def test_veltkamp_split_is_round_to_nearest_even_on_whole_binades():
 
 def test_veltkamp_split_keeps_short_values():
     """Values with at most 10 significant bits (e.g. FP16 subnormal sums,
-    k * 2^-39 with k < 512, scaled by 2^64) pass through unchanged."""
+    k * 2^-39 with k < 512) pass through unchanged."""
     k = np.arange(1, 1 << 10, dtype=np.float64)
-    for scale in (2.0 ** 25, 2.0 ** 40, 2.0 ** 70):
+    for scale in (2.0 ** -39, 2.0 ** -20, 2.0 ** 10):
         x = (k * scale).astype(np.float32)
         assert np.array_equal(veltkamp10(x), x)
         assert np.array_equal(veltkamp10(-x), -x)
