@@ -70,8 +70,8 @@ def lib():
                                             vp, vp, i64, vp]
         L.cpu_chunk_gemm_fast_bounds_points.restype = ctypes.c_int
         L.cpu_chunk_gemm_fast_bounds_points.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64,
-                                                        i64, i64, vp, i64, vp, i64, vp, vp,
-                                                        i64, vp, vp]
+                                                        i64, i64, vp, i64, vp, i64,
+                                                        ctypes.c_int, vp, vp, i64, vp, vp]
         u32 = ctypes.c_uint32
         L.cpu_chunk_gemm_sr.restype = ctypes.c_int
         L.cpu_chunk_gemm_sr.argtypes = [ctypes.c_int, ctypes.c_int, i64, i64, i64, i64,
@@ -230,9 +230,12 @@ def chunk_gemm_points(A, B, CL, rows, cols, trans_a=0, trans_b=0, mode=EXACT):
     return out
 
 
-def chunk_gemm_fast_bounds(A, B, CL, trans_a=0, trans_b=0, rows=None, cols=None):
+def chunk_gemm_fast_bounds(A, B, CL, trans_a=0, trans_b=0, rows=None, cols=None, *,
+                           matrix_core):
     """(lo, hi) P16 codes bounding the fast mode's result at every output
-    (rows, cols None: the whole M x N matrix, else the listed outputs)."""
+    (rows, cols None: the whole M x N matrix, else the listed outputs), for
+    chunk sums on the FP8 matrix cores (matrix_core=True) or in FP32 on the
+    vector ALUs."""
     A = np.ascontiguousarray(A, dtype=np.uint8)
     B = np.ascontiguousarray(B, dtype=np.uint8)
     M, N, K = _gemm_dims(trans_a, trans_b, A, B)
@@ -247,7 +250,8 @@ def chunk_gemm_fast_bounds(A, B, CL, trans_a=0, trans_b=0, rows=None, cols=None)
     ldb = B.shape[1] if B.shape[1] > 0 else 1
     _check(lib().cpu_chunk_gemm_fast_bounds_points(int(trans_a), int(trans_b), M, N, K,
                                                    int(CL), _ptr(A), lda, _ptr(B), ldb,
-                                                   _ptr(rows), _ptr(cols), rows.size,
+                                                   int(bool(matrix_core)), _ptr(rows),
+                                                   _ptr(cols), rows.size,
                                                    _ptr(lo), _ptr(hi)),
            "chunk_gemm_fast_bounds")
     return lo.reshape(shape), hi.reshape(shape)

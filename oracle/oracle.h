@@ -66,15 +66,17 @@ int cpu_chunk_gemm_points(int trans_a, int trans_b, int64_t M, int64_t N,
                           const int64_t* rows, const int64_t* cols,
                           int64_t npts, uint16_t* out);
 
-/* Bounds on what the fast mode may give at the outputs (rows[p], cols[p]):
- * every chunk's FP32 sum of n products, in any order, within
- * n 2^-22 / (1 - n 2^-22) sum|p| of the exact one; lo[p] and hi[p] are the
- * two monotone chains of ops.c.  Requires min(CL, K) <= 2^21. */
+/* Bounds on what the fast mode may give at the outputs (rows[p], cols[p]),
+ * defined in ops.c: chunk sums in FP32 on the vector ALUs (matrix_core = 0)
+ * or on the FP8 matrix cores with their measured group truncation
+ * (matrix_core = 1); lo[p] and hi[p] are the two monotone FP16 chains.
+ * Requires min(CL, K) <= 2^21. */
 int cpu_chunk_gemm_fast_bounds_points(int trans_a, int trans_b, int64_t M, int64_t N,
                                       int64_t K, int64_t CL, const uint8_t* A,
                                       int64_t lda, const uint8_t* B, int64_t ldb,
-                                      const int64_t* rows, const int64_t* cols,
-                                      int64_t npts, uint16_t* lo, uint16_t* hi);
+                                      int matrix_core, const int64_t* rows,
+                                      const int64_t* cols, int64_t npts, uint16_t* lo,
+                                      uint16_t* hi);
 
 /* chunk_gemm with stochastic instead of nearest rounding after every P16
  * addition (Sec. 2.3, Fig. 3(b)); random bits keyed by (seed, i, j, k) as
