@@ -16,7 +16,9 @@
  * Conventions for every call:
  *   - All array pointers are device pointers owned by the caller.  The
  *     library never allocates, frees or synchronizes; work is enqueued on
- *     `stream` (0 = the null stream) and runs asynchronously.
+ *     `stream` (0 = the null stream) and runs asynchronously.  (The one
+ *     device array it owns, chunk_gemm_noalloc's scratch, is a static
+ *     array of its code object.)
  *   - Arguments are validated before anything is enqueued.  A call that
  *     returns an error has enqueued nothing.
  *   - Sizes are element counts.  Matrices are row-major with a leading
@@ -130,6 +132,29 @@ int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
  */
 size_t chunk_gemm_workspace_size(int trans_a, int trans_b, int64_t M,
                                  int64_t N, int64_t K, int64_t CL, int mode);
+
+/*
+ * chunk_gemm_noalloc -- chunk_gemm for callers that cannot allocate device
+ * memory or pass a workspace (code under stream or graph capture, tight
+ * serving loops, harnesses that forbid allocation).  Same arguments as
+ * chunk_gemm without the workspace, same results bit for bit (the result
+ * does not depend on the plan).  The chunk sums of shared tiles go to a
+ * library-owned device array of FP8T_NOALLOC_SCRATCH_BYTES per GPU, a static
+ * array of the library's code object that each GPU holds until the process
+ * ends; the call takes the fastest plan whose chunk sums fit in it (a plan
+ * without shared tiles needs none, so every valid call runs) and calls no
+ * allocating routine.  Every call on one GPU uses that GPU's array: calls
+ * whose execution overlaps on one GPU (different streams, not ordered by
+ * events) race and may give wrong results; stream-ordered calls are safe.
+ * Nothing in the array needs to start at zero.
+ * Errors: as chunk_gemm (without the workspace cases); FP8T_EHIP also when
+ * the array's device address cannot be obtained.
+ */
+#define FP8T_NOALLOC_SCRATCH_BYTES (64u * 1024u * 1024u)
+int chunk_gemm_noalloc(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                       int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+                       int64_t ldb, uint16_t* C, int64_t ldc, int mode,
+                       hipStream_t stream);
 
 /*
  * chunk_gemm_fp8 -- chunk_gemm with the result also rounded back to FP8 in

@@ -43,6 +43,9 @@ def lib():
         L.chunk_gemm.restype = i32
         L.chunk_gemm.argtypes = [i32, i32, i64, i64, i64, i64, vp, i64, vp, i64, vp, i64,
                                  i32, vp, sz, vp]
+        L.chunk_gemm_noalloc.restype = i32
+        L.chunk_gemm_noalloc.argtypes = [i32, i32, i64, i64, i64, i64, vp, i64, vp, i64, vp, i64,
+                                         i32, vp]
         L.chunk_gemm_workspace_size.restype = sz
         L.chunk_gemm_workspace_size.argtypes = [i32, i32, i64, i64, i64, i64, i32]
         L.chunk_gemm_fp8.restype = i32
@@ -156,6 +159,17 @@ def chunk_gemm(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, mode=EXACT
                                           int(CL), _ptr(A), int(lda), _ptr(B), int(ldb),
                                           _ptr(C), int(ldc), int(mode), _ptr(workspace),
                                           int(workspace_bytes), _stream(stream)))
+    return C
+
+
+def chunk_gemm_noalloc(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, mode=EXACT,
+                       stream=None):
+    """The C-ABI call with the same argument order (no workspace: the
+    library's static scratch holds shared tiles' chunk sums)."""
+    _check("chunk_gemm_noalloc",
+           lib().chunk_gemm_noalloc(int(trans_a), int(trans_b), int(M), int(N), int(K), int(CL),
+                                    _ptr(A), int(lda), _ptr(B), int(ldb), _ptr(C), int(ldc),
+                                    int(mode), _stream(stream)))
     return C
 
 

@@ -217,9 +217,10 @@ struct Choice {
 constexpr size_t kWsAlign = 256;
 
 // The best kernel configuration and work decomposition for these sizes; with
-// allow_ws false only plans that need no workspace are considered.
+// allow_ws false only plans that need no workspace are considered, otherwise
+// only plans whose workspace is at most ws_cap bytes.
 Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL,
-                 bool allow_ws, bool conv = false) {
+                 bool allow_ws, bool conv = false, size_t ws_cap = SIZE_MAX) {
     Choice best;
     const int cus = device_cus();
     if (cus <= 0) return best;
@@ -300,6 +301,7 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                     const int64_t wg_per_cu = (G + cus - 1) / cus;
                     const int64_t per_wg = q * nch + (p.L + G - 1) / G;
                     ws = (size_t)(T - p.t_whole) * nch * BM * BN * sizeof(uint16_t) + kWsAlign;
+                    if (ws > ws_cap) continue;
                     est = (double)wg_per_cu * (per_wg * t_chunk + (q + 2) * t_tile) +
                           2.0 * (double)ws / kFoldBytesPerS + 4e-6;
                 }
@@ -345,6 +347,38 @@ int launch_plan(const Choice& ch, GemmArgs g, hipStream_t stream) {
 
 using namespace fp8t;
 
+// ---------------------------------------------------------------------------
+// scratch of chunk_gemm_noalloc
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// The chunk sums of shared tiles for chunk_gemm_noalloc: one array per GPU,
+// held by the loaded code object until the process ends.  Nothing in it needs
+// to start at zero: a call's fold reads only chunk sums its own GEMM kernel
+// wrote before, in stream order.  Calls that overlap in time on one GPU
+// share the array and race.
+__device__ __align__(256) uint8_t scratch[FP8T_NOALLOC_SCRATCH_BYTES];
+
+// The device address of `scratch` on each GPU, taken once per device with
+// that device current.  In host code `scratch` names a host-side stand-in,
+// so only this address may be handed to kernels.
+void* scratch_address() {
+    static std::mutex mu;
+    static void* ptr[64] = {nullptr};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        ptr[dev] = p;
+    }
+    return ptr[dev];
+}
+
+}  // namespace
+
 namespace {
 bool gemm_args_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, int mode) {
     if (M < 0 || N < 0 || K < 0 || CL < 1) return false;
@@ -381,7 +415,8 @@ size_t workspace_query(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t 
 int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t CL,
               const uint8_t* A, int64_t lda, const uint8_t* B, int64_t ldb, uint16_t* C,
               int64_t ldc, uint8_t* C8, int64_t ldc8, float scale, int mode, void* workspace,
-              size_t workspace_bytes, hipStream_t stream, bool fp8out) {
+              size_t workspace_bytes, hipStream_t stream, bool fp8out,
+              bool use_scratch = false) {
     if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, mode)) return FP8T_EINVAL;
     if (M == 0 || N == 0) return FP8T_OK;
     if (!fp8out && !C) return FP8T_EINVAL;
@@ -392,6 +427,11 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
         if (lda < (trans_a ? M : K) || ldb < (trans_b ? K : N)) return FP8T_EINVAL;
     }
     if (workspace_bytes > 0 && !workspace) return FP8T_EINVAL;
+    if (use_scratch) {                    // after validation: nothing touched the GPU yet
+        workspace = scratch_address();
+        if (!workspace) return FP8T_EHIP;
+        workspace_bytes = FP8T_NOALLOC_SCRATCH_BYTES;
+    }
     if (CL > K && K > 0) CL = K;           // one chunk
     const int m = (int)M, n = (int)N, k = (int)K, cl = (int)(K > 0 ? CL : 1);
     if (K == 0) {
@@ -401,9 +441,11 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
         return launch_status();
     }
     // With no workspace, the best plan that needs none; with one, the best
-    // plan overall, which must then fit.
+    // plan overall, which must then fit; with the scratch, the best plan that
+    // fits in it.
     const Choice ch = plan_gemm(kind_of(mode, K, cl), trans_a, trans_b, M, N, K, cl,
-                                workspace_bytes > 0);
+                                workspace_bytes > 0, false,
+                                use_scratch ? workspace_bytes : SIZE_MAX);
     if (ch.cfg < 0) return FP8T_EHIP;
     if (plan_workspace(ch, fp8out) > workspace_bytes) return FP8T_EWORKSPACE;
     GemmArgs g{};
@@ -453,6 +495,14 @@ extern "C" int chunk_gemm(int trans_a, int trans_b, int64_t M, int64_t N, int64_
                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
     return gemm_call(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, nullptr, 0, 1.0f,
                      mode, workspace, workspace_bytes, stream, false);
+}
+
+extern "C" int chunk_gemm_noalloc(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                                  int64_t CL, const uint8_t* A, int64_t lda, const uint8_t* B,
+                                  int64_t ldb, uint16_t* C, int64_t ldc, int mode,
+                                  hipStream_t stream) {
+    return gemm_call(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, nullptr, 0, 1.0f,
+                     mode, nullptr, 0, stream, false, true);
 }
 
 extern "C" size_t chunk_gemm_fp8_workspace_size(int trans_a, int trans_b, int64_t M,

@@ -33,6 +33,7 @@ def lib():
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted([
         "fp8_quantize", "fp16_quantize", "chunk_gemm", "chunk_gemm_workspace_size",
+        "chunk_gemm_noalloc",
         "chunk_gemm_fp8", "chunk_gemm_fp8_workspace_size",
         "chunk_gemm_sr", "chunk_gemm_sr_workspace_size", "adam_update",
         "chunk_gemm_p16", "chunk_gemm_p16_workspace_size",
@@ -96,6 +97,23 @@ def test_chunk_gemm_rejects(lib):
     assert _gemm(lib, K=2 ** 31 - 4096, lda=2 ** 31) == E
     assert _gemm(lib, M=0) == fp8t.OK                   # empty output: no-op
     assert _gemm(lib, N=0, C=None) == fp8t.OK
+
+
+def test_chunk_gemm_noalloc_rejects(lib):
+    """Validation comes before the scratch's device address is taken, so the
+    rejections need no GPU."""
+    def call(**kw):
+        a = dict(ta=0, tb=0, M=4, N=4, K=4, CL=2, A=FAKE, lda=4, B=FAKE, ldb=4, C=FAKE, ldc=4,
+                 mode=0)
+        a.update(kw)
+        return lib.chunk_gemm_noalloc(a["ta"], a["tb"], a["M"], a["N"], a["K"], a["CL"], a["A"],
+                                      a["lda"], a["B"], a["ldb"], a["C"], a["ldc"], a["mode"],
+                                      None)
+    E = fp8t.EINVAL
+    for kw in (dict(CL=0), dict(M=-1), dict(ta=2), dict(mode=3), dict(lda=3), dict(ldb=3),
+               dict(ldc=3), dict(A=None), dict(C=None), dict(M=2 ** 31)):
+        assert call(**kw) == E, kw
+    assert call(M=0) == fp8t.OK
 
 
 def _gemm8(lib, **kw):
