@@ -254,6 +254,208 @@ def extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16):
     return out
 
 
+def valu_fast_peak_mac_s(cl):
+    """Fast mode for chunks the matrix cores cannot split (CL not a multiple
+    of 16): an FP32 FMA per MAC plus the 8-op epilogue per output per chunk."""
+    return VALU_LANE_OPS / (1.0 + 8.0 / cl)
+
+
+def mode_peak(mode_fast, cl, K=None):
+    """Ceiling of a chunk_gemm call: CL = 1 is the single chain of CL = K in
+    both modes (a one-product chunk is exact), priced as that."""
+    if cl == 1 and K:
+        return exact_peak_mac_s(K), "valu_emulation"
+    if not mode_fast:
+        return exact_peak_mac_s(cl), "valu_emulation"
+    if cl % 16 == 0:
+        return fast_peak_mac_s(cl), "min(fp8_mfma, valu_epilogue)"
+    return valu_fast_peak_mac_s(cl), "valu_fp32"
+
+
+def _p8_table():
+    """FP8 (1,5,2) values of all 256 codes from the bit fields (bias 15,
+    subnormals, Inf/NaN at exponent 31), for the error metric."""
+    v = []
+    for c in range(256):
+        e, m = (c >> 2) & 31, c & 3
+        x = float("nan") if e == 31 and m else float("inf") if e == 31 else \
+            (m / 4.0) * 2.0 ** -14 if e == 0 else (1 + m / 4.0) * 2.0 ** (e - 15)
+        v.append(-x if c & 0x80 else x)
+    return v
+
+
+def _p16_table():
+    """FP16 (1,6,9) values of all 65536 codes from the bit fields (bias 31),
+    for the error metric."""
+    c = np.arange(65536, dtype=np.int64)
+    e, m = (c >> 9) & 63, c & 511
+    mag = np.where(e == 0, m * 2.0 ** -39, (512 + m) * np.exp2(np.maximum(e, 1) - 40.0))
+    mag = np.where(e == 63, np.where(m == 0, np.inf, np.nan), mag)
+    return np.where(c & 0x8000, -mag, mag)
+
+
+def gemm_case(torch, fp8t, A, B, M, N, K, cl, ta, tb, reps):
+    """ms, TMAC/s and fraction of each mode's ceiling of one GEMM shape."""
+    C = torch.empty((M, N), dtype=torch.uint16, device="cuda")
+    row = {}
+    for mode, tag in ((0, "exact"), (1, "fast")):
+        wb = fp8t.chunk_gemm_workspace_size(ta, tb, M, N, K, cl, mode)
+        ws = torch.empty(wb, dtype=torch.uint8, device="cuda") if wb else None
+        ms = time_ms(torch, lambda: fp8t.chunk_gemm(ta, tb, M, N, K, cl, A, A.shape[1], B,
+                                                    B.shape[1], C, N, mode, ws, wb), reps)
+        peak, kind = mode_peak(mode == 1, min(cl, K), K)
+        rate = M * N * K / (ms * 1e-3)
+        row[tag] = {"ms": ms, "tmac_s": rate / 1e12, "frac": rate / peak, "bound": kind,
+                    "workspace_mb": wb / 1e6}
+        del ws
+    return row, C
+
+
+def sweep_measurement(torch, fp8t):
+    """The long-accumulation sweep (weight-gradient layout, 512 x 512 outputs,
+    K in {4096, 16384, 65536} x CL in {1, 8, 64, 256, K}): per mode the time,
+    rate and fraction of the mode's ceiling, and the normalized L2 error of
+    the FP16 result against float64 dot products of the same FP8 operands
+    (Sec. 2.3 Fig. 3(b), Sec. 4.2 Fig. 6: swamping at CL = 1 and CL = K,
+    chunking in between)."""
+    import workloads
+    p8 = torch.tensor(_p8_table(), dtype=torch.float64, device="cuda")
+    p16 = torch.tensor(_p16_table(), dtype=torch.float64, device="cuda")
+    res = {}
+    for K in workloads.SWEEP_K:
+        A32, B32 = workloads.sweep_gemm(K)
+        A8 = torch.empty(A32.shape, dtype=torch.uint8, device="cuda")
+        B8 = torch.empty(B32.shape, dtype=torch.uint8, device="cuda")
+        fp8t.fp8_quantize(torch.from_numpy(A32).cuda(), A8)
+        fp8t.fp8_quantize(torch.from_numpy(B32).cuda(), B8)
+        Af, Bf = p8[A8.long()], p8[B8.long()]
+        ref = Af.t() @ Bf                  # float64: the products are exact
+        del Af, Bf
+        ref_norm = torch.linalg.vector_norm(ref).item()
+        for cl in (1, 8, 64, 256, K):
+            C = torch.empty((512, 512), dtype=torch.uint16, device="cuda")
+            row = {}
+            for mode, tag in ((0, "exact"), (1, "fast")):
+                wb = fp8t.chunk_gemm_workspace_size(1, 0, 512, 512, K, cl, mode)
+                ws = torch.empty(wb, dtype=torch.uint8, device="cuda") if wb else None
+                ms = time_ms(torch, lambda: fp8t.chunk_gemm(1, 0, 512, 512, K, cl, A8, 512, B8,
+                                                            512, C, 512, mode, ws, wb), 3)
+                peak, kind = mode_peak(mode == 1, min(cl, K), K)
+                rate = 512 * 512 * K / (ms * 1e-3)
+                got = p16[C.view(torch.int16).long() & 0xFFFF]
+                err = torch.linalg.vector_norm(got - ref).item() / ref_norm
+                row[tag] = {"ms": ms, "tmac_s": rate / 1e12, "frac": rate / peak, "bound": kind,
+                            "l2_err_vs_f64": err}
+                del ws
+            res[f"K{K}_CL{'K' if cl == K else cl}"] = row
+        del ref
+    return res
+
+
+def small_measurement(torch, fp8t):
+    """The small case: one 128 x 128 x 1024 GEMM (CL 64) and a 4096-element
+    update -- launch-bound, so the time per call over many back-to-back calls
+    (HIP events) is reported."""
+    import workloads
+    A32, B32, s = workloads.small_gemm()
+    A8 = torch.empty(A32.shape, dtype=torch.uint8, device="cuda")
+    B8 = torch.empty(B32.shape, dtype=torch.uint8, device="cuda")
+    fp8t.fp8_quantize(torch.from_numpy(A32).cuda(), A8, s)
+    fp8t.fp8_quantize(torch.from_numpy(B32).cuda(), B8, s)
+    C = torch.empty((128, 128), dtype=torch.uint16, device="cuda")
+    res = {}
+    for mode, tag in ((0, "exact"), (1, "fast")):
+        ms = time_ms(torch, lambda: fp8t.chunk_gemm(0, 0, 128, 128, 1024, CL, A8, 1024, B8, 128,
+                                                    C, 128, mode), 200)
+        res[f"gemm_{tag}_us"] = ms * 1e3
+        res[f"gemm_{tag}_tmac_s"] = 128 * 128 * 1024 / (ms * 1e-3) / 1e12
+    u = workloads.small_update()
+    w16 = torch.empty(4096, dtype=torch.uint16, device="cuda")
+    g16 = torch.empty(4096, dtype=torch.uint16, device="cuda")
+    w8 = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    fp8t.fp16_quantize(torch.from_numpy(u["w"]).cuda(), w16)
+    fp8t.fp16_quantize(torch.from_numpy(u["g"]).cuda(), g16)
+    ms = time_ms(torch, lambda: fp8t.sr_weight_update(w16, g16, None, w8, 4096, u["lr"], 0.0,
+                                                      0.0, u["seed"], 0), 200)
+    res["sr_update_us"] = ms * 1e3
+    return res
+
+
+def speech_layers_measurement(torch, fp8t):
+    """The speech DNN's 18 GEMMs at batch 256 (layers 440 -> 1024, four
+    1024 -> 1024, 1024 -> 6000; forward, backward-data and weight-gradient
+    each, CL 64) on their own, both modes."""
+    import workloads
+    res, macs = {}, 0
+    for l, (fi, fo) in enumerate(workloads.SPEECH_LAYERS):
+        d = workloads.speech_layer(l)
+        X8 = torch.empty(d["X"].shape, dtype=torch.uint8, device="cuda")
+        W8 = torch.empty(d["W"].shape, dtype=torch.uint8, device="cuda")
+        E8 = torch.empty(d["E"].shape, dtype=torch.uint8, device="cuda")
+        fp8t.fp8_quantize(torch.from_numpy(d["X"]).cuda(), X8)
+        fp8t.fp8_quantize(torch.from_numpy(d["W"]).cuda(), W8)
+        fp8t.fp8_quantize(torch.from_numpy(d["E"]).cuda(), E8, d["e_scale"])
+        B = d["X"].shape[0]
+        for g, (A, Bm, M, N, K, ta, tb) in (("fwd", (X8, W8, B, fo, fi, 0, 0)),
+                                           ("dgrad", (E8, W8, B, fi, fo, 0, 1)),
+                                           ("wgrad", (X8, E8, fi, fo, B, 1, 0))):
+            res[f"L{l}_{fi}x{fo}_{g}"], _ = gemm_case(torch, fp8t, A, Bm, M, N, K, CL, ta, tb, 20)
+            macs += M * N * K
+    tot = {}
+    for tag in ("exact", "fast"):
+        ms = sum(r[tag]["ms"] for r in res.values())
+        tot[tag] = {"ms": ms, "tmac_s": macs / (ms * 1e-3) / 1e12,
+                    "frac": macs / (ms * 1e-3) / mode_peak(tag == "fast", CL)[0]}
+    res["all_18"] = tot
+    return res
+
+
+def cpu_baseline_configs(target_s=2.0):
+    """The oracle timed beside the other configurations (all host cores, a
+    bounded sample each): the small GEMM and update in full, and sampled
+    outputs of the sweep (K 16384, CL 64 and 1) and of the speech DNN's
+    largest GEMMs (1024 -> 6000 layer)."""
+    import oracle
+    import workloads
+    out = {}
+    A32, B32, s = workloads.small_gemm()
+    Ao, Bo = oracle.fp8_quantize(A32, s), oracle.fp8_quantize(B32, s)
+    t0 = time.perf_counter()
+    oracle.chunk_gemm(Ao, Bo, CL)
+    t = time.perf_counter() - t0
+    out["small_gemm_exact"] = {"us": t * 1e6, "gmac_s": 128 * 128 * 1024 / t / 1e9}
+    u = workloads.small_update()
+    wo, go = oracle.fp16_quantize(u["w"]), oracle.fp16_quantize(u["g"])
+    t0 = time.perf_counter()
+    oracle.sr_weight_update(wo, go, None, lr=u["lr"], seed=u["seed"])
+    out["small_sr_update_us"] = (time.perf_counter() - t0) * 1e6
+
+    def rate(name, A, B, M, N, K, cl, ta, tb, mode):
+        rng = np.random.default_rng(98)
+        npts = 4
+        while True:
+            r, c = rng.integers(0, M, npts), rng.integers(0, N, npts)
+            t0 = time.perf_counter()
+            oracle.chunk_gemm_points(A, B, cl, r, c, ta, tb, mode=mode)
+            t = time.perf_counter() - t0
+            if t > 0.25 * target_s or npts >= 1 << 16:
+                break
+            npts *= 4
+        out[name] = {"gmac_s": npts * K / t / 1e9, "sample_outputs": npts}
+
+    A32, B32 = workloads.sweep_gemm(16384)
+    Ao, Bo = oracle.fp8_quantize(A32), oracle.fp8_quantize(B32)
+    rate("sweep_K16384_CL64_exact", Ao, Bo, 512, 512, 16384, 64, 1, 0, oracle.EXACT)
+    rate("sweep_K16384_CL1_exact", Ao, Bo, 512, 512, 16384, 1, 1, 0, oracle.EXACT)
+    rate("sweep_K16384_CL64_fast", Ao, Bo, 512, 512, 16384, 64, 1, 0, oracle.FAST)
+    d = workloads.speech_layer(5)
+    Xo, Wo = oracle.fp8_quantize(d["X"]), oracle.fp8_quantize(d["W"])
+    Eo = oracle.fp8_quantize(d["E"], d["e_scale"])
+    rate("speech_L5_fwd_exact", Xo, Wo, 256, 6000, 1024, CL, 0, 0, oracle.EXACT)
+    rate("speech_L5_wgrad_exact", Xo, Eo, 1024, 6000, 256, CL, 1, 0, oracle.EXACT)
+    return out
+
+
 def conv_measurement(torch, fp8t, W8, D8, u8, u16):
     """The conv stage's Forward and Gradient GEMMs reading the NHWC input
     directly (no lowered matrix in memory), and col2im of the lowered error."""
@@ -452,8 +654,13 @@ def main():
     }
     if not args.no_extras:
         result["kernels"].update(extra_measurements(torch, fp8t, X8, D8, W8, M, N, K, u8, u16))
+        result["kernels"]["small"] = small_measurement(torch, fp8t)
+        result["kernels"]["sweep"] = sweep_measurement(torch, fp8t)
+        result["kernels"]["speech_layers"] = speech_layers_measurement(torch, fp8t)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(work, args.cpu_seconds)
+        if not args.no_extras:
+            result["cpu_baseline"]["configs"] = cpu_baseline_configs()
     print(json.dumps(result), flush=True)
 
 

@@ -169,10 +169,11 @@ constexpr double kClockHz = 2.4e9;      // MI355X peak engine clock
 constexpr double kLanesPerCU = 128.0;   // 32-bit VALU lane-ops per clock per CU
 constexpr double kFoldBytesPerS = 5e12; // effective HBM rate of the fold pass
 
-// Relative cost per multiply-accumulate of each register tile on a fully
-// loaded CU, in VALU instructions (4 for the rounded FMA of the guarded path,
-// plus operand decode, LDS reads, loop overhead and lost occupancy; measured
-// on the conv-stage GEMMs for the large tiles).
+// Relative cost per multiply-accumulate of each register tile on a CU with
+// enough waves resident (see valu_efficiency), in VALU instructions (4 for
+// the rounded FMA of the guarded path, plus operand decode, LDS reads and
+// loop overhead; measured on the conv-stage GEMMs for the large tiles, on
+// the 512 x 512 long-accumulation GEMMs for the small ones).
 double valu_ops_per_mac(int cfg) {
     switch (cfg) {
         case 4: return 4.6;     // 4 x 4, 4 waves per SIMD
@@ -182,10 +183,20 @@ double valu_ops_per_mac(int cfg) {
         case 0: return 5.2;
         case 7: return 4.3;     // 4 x 4 on 128 x 64 tiles, 8 waves per workgroup
         case 8: return 4.3;     // 4 x 4 on 64 x 128 tiles, 8 waves per workgroup
-        case 5: return 6.5;     // 2 x 2
-        default: return 10.0;   // 1 x 1
+        case 5: return 7.0;     // 2 x 2
+        case kChainConfig: return 6.0;       // chain kernel, 2 x 2
+        case kChainConfig + 1: return 6.1;   // chain kernel, 1 x 2
+        case kChainConfig + 2: return 9.0;   // chain kernel, 1 x 1
+        default: return 10.8;   // 1 x 1
     }
 }
+
+// Fraction of a CU's VALU rate reached with w waves per SIMD resident: each
+// multiply-accumulate is a chain of four dependent instructions, and on
+// gfx950 about four waves per SIMD are needed to issue every cycle whatever
+// the outputs per lane (measured: a 2 x 2 register tile at one wave per SIMD
+// runs at a quarter of the rate a 1 x 1 tile reaches at four).
+double valu_efficiency(double w) { return w >= 4.0 ? 1.0 : w / 4.0; }
 
 // Matrix-core fast mode, CU time of one output-chunk (the VALU epilogue
 // dominates; the matrix-core share grows with CL) and of the per-tile start
@@ -252,10 +263,13 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 t_out = mfma_cost_per_output_chunk(cfg, CL);
                 t_tile = mfma_cost_per_tile(cfg);
             } else {
+                // the chain kernel: exact mode, 4-k groups inside one chunk
+                if (is_chain(cfg) && (fast || conv || (CL % 4 != 0 && CL < K))) continue;
                 const ValuShape sh = valu_shape(cfg);
                 fn = conv ? valu_conv_kernel(cfg, ta) : valu_kernel(cfg, ta, tb, fast);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
-                t_out = (double)CL * valu_ops_per_mac(cfg) / (kLanesPerCU * kClockHz);
+                // the MACs of a chunk, and its end (an add and a rounding)
+                t_out = ((double)CL * valu_ops_per_mac(cfg) + 4.0) / (kLanesPerCU * kClockHz);
             }
             if (!fn) continue;
             int occ = kernel_occupancy(fn, NT);
@@ -277,8 +291,9 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 size_t ws = 0;
                 // the streamed kernel writes split tiles' chunk sums as scattered
                 // 2-byte stores: the other kernels are faster there; the
-                // chunk-per-wave kernel has no shared tiles
+                // chunk-per-wave and chain kernels have no shared tiles
                 if (split && mf && cfg >= 2) continue;
+                if (split && !mf && is_chain(cfg)) continue;
                 if (!split) {
                     const int64_t G = T < gmax ? T : gmax;
                     p.G = (int)G;
@@ -290,6 +305,10 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                     int64_t per_cu = (T + cus - 1) / cus;
                     if (mf && cfg == 2 && per_cu < 2) per_cu = 2;
                     est = (double)per_cu * (nch * t_chunk + t_tile);
+                    if (!mf) {
+                        const int64_t res = per_cu < occ ? per_cu : occ;
+                        est /= valu_efficiency((double)res * NT / 256.0);
+                    }
                 } else {
                     int64_t G = gmax;
                     if (G > T * nch) G = T * nch;
@@ -302,8 +321,12 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                     const int64_t per_wg = q * nch + (p.L + G - 1) / G;
                     ws = (size_t)(T - p.t_whole) * nch * BM * BN * sizeof(uint16_t) + kWsAlign;
                     if (ws > ws_cap) continue;
-                    est = (double)wg_per_cu * (per_wg * t_chunk + (q + 2) * t_tile) +
-                          2.0 * (double)ws / kFoldBytesPerS + 4e-6;
+                    est = (double)wg_per_cu * (per_wg * t_chunk + (q + 2) * t_tile);
+                    if (!mf) {
+                        const int64_t res = wg_per_cu < occ ? wg_per_cu : occ;
+                        est /= valu_efficiency((double)res * NT / 256.0);
+                    }
+                    est += 2.0 * (double)ws / kFoldBytesPerS + 4e-6;
                 }
                 p.xcd_remap = p.t_whole % 8 == 0 && p.G % 8 == 0;
                 if (force_split == 1 && !split && allow_ws) est *= 1e6;   // any shared plan wins
@@ -389,6 +412,16 @@ bool gemm_args_ok(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, i
     return true;
 }
 
+// CL = 1 is the plain sequential FP16 sum in both modes (a one-product chunk
+// is exact, also when summed in FP32), the same chain as one chunk of K in
+// exact mode: run it that way.
+void normalize_chunking(int& mode, int64_t K, int64_t& CL) {
+    if (CL == 1 && K > 1) {
+        CL = K;
+        mode = FP8T_EXACT;
+    }
+}
+
 Kind kind_of(int mode, int64_t K, int64_t CL) {
     const int64_t cl = CL > K ? K : CL;
     if (mode == FP8T_EXACT) return VALU_EXACT;
@@ -408,6 +441,7 @@ size_t workspace_query(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t 
                        bool fp8out) {
     if (!gemm_args_ok(ta, tb, M, N, K, CL, mode)) return 0;
     if (M == 0 || N == 0 || K == 0) return 0;
+    normalize_chunking(mode, K, CL);
     const int64_t cl = CL > K ? K : CL;
     return plan_workspace(plan_gemm(kind_of(mode, K, cl), ta, tb, M, N, K, cl, true), fp8out);
 }
@@ -432,6 +466,7 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
         if (!workspace) return FP8T_EHIP;
         workspace_bytes = FP8T_NOALLOC_SCRATCH_BYTES;
     }
+    normalize_chunking(mode, K, CL);
     if (CL > K && K > 0) CL = K;           // one chunk
     const int m = (int)M, n = (int)N, k = (int)K, cl = (int)(K > 0 ? CL : 1);
     if (K == 0) {
@@ -478,6 +513,7 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     g.c_vec = C && aligned(C, 4) && ldc % 2 == 0;
     g.c_vec16 = C && aligned(C, 16) && ldc % 8 == 0;
     g.c8_vec8 = C8 && aligned(C8, 8) && ldc8 % 8 == 0;
+    g.c8_vec4 = C8 && aligned(C8, 4) && ldc8 % 4 == 0;
     // FP8T_GEMM_GUARD=0 runs every piece on the safe path (tests, tuning).
     g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
     return launch_plan(ch, g, stream);

@@ -56,6 +56,7 @@ struct GemmArgs {
     int c_vec;          // C, ldc allow 4-byte stores of code pairs
     int c_vec16;        // C, ldc allow 16-byte stores (8 codes)
     int c8_vec8;        // C8, ldc8 allow 8-byte stores
+    int c8_vec4;        // C8, ldc8 allow 4-byte stores
     int guarded;        // exact mode: try the guarded path first
     ConvGeom conv;      // A is the implicit lowering of an NHWC input (conv kernels)
 };

@@ -12,7 +12,13 @@ struct ValuShape {
     int NT;         // threads per workgroup
 };
 
-constexpr int kValuConfigs = 9;
+// Configurations 0-8 are chunk_gemm_valu register tiles (gemm_valu_impl.h);
+// configurations 9, 10, 11 are chunk_gemm_chain (gemm_chain.hip) with 2 x 2,
+// 1 x 2 and 1 x 1 outputs per lane: exact mode only, whole tiles, CL a
+// multiple of 4 or covering K.
+constexpr int kValuConfigs = 12;
+constexpr int kChainConfig = 9;
+inline bool is_chain(int cfg) { return cfg >= kChainConfig && cfg < kChainConfig + 3; }
 
 ValuShape valu_shape(int cfg);
 
@@ -27,5 +33,9 @@ const void* valu_kernel(int cfg, int ta, int tb, int fast);
 // lowered convolution input (GemmArgs::conv); trans_b = 0; null where not
 // built (only configuration 4).
 const void* valu_conv_kernel(int cfg, int ta);
+
+// chunk_gemm_chain with 2 x 2 (shape 0), 1 x 2 (1) or 1 x 1 (2) outputs per
+// lane for the given operand layouts (gemm_chain.hip).
+const void* chain_kernel(int shape, int ta, int tb);
 
 }  // namespace fp8t

@@ -18,12 +18,16 @@ ValuShape valu_shape(int cfg) {
         case 5: return valu_impl::shape_of<5>();
         case 7: return valu_impl::shape_of<7>();
         case 8: return valu_impl::shape_of<8>();
+        case kChainConfig: return ValuShape{2, 2, 32, 32, 256};
+        case kChainConfig + 1: return ValuShape{1, 2, 16, 32, 256};
+        case kChainConfig + 2: return ValuShape{1, 1, 16, 16, 256};
         default: return valu_impl::shape_of<6>();
     }
 }
 
 const void* valu_kernel(int cfg, int ta, int tb, int fast) {
     if (cfg < 0 || cfg >= kValuConfigs) return nullptr;
+    if (is_chain(cfg)) return fast ? nullptr : chain_kernel(cfg - kChainConfig, ta, tb);
     if (!ta && !tb) return valu_kernel_nn(cfg, fast);
     if (!ta && tb) return valu_kernel_nt(cfg, fast);
     if (ta && !tb) return valu_kernel_tn(cfg, fast);

@@ -13,13 +13,15 @@
 //   * guarded (default): plain values, rounding by Veltkamp splitting
 //     (rn16v: v_mul, v_sub, v_sub) -- 4 full-rate instructions per
 //     multiply-accumulate (FP16 subnormals are FP32-normal, so no scaling is
-//     needed when nothing can overflow).  It holds when no operand is Inf/NaN and no
-//     partial sum can reach the FP16 overflow threshold: every partial sum of
-//     the two-level chain is at most 9 sum_k |a_k b_k| (an RN step adds at
-//     most 3x its non-negative addend, over two levels), so
-//     9 K max|a| max|b| < 2^31 suffices.  Each workgroup tracks the largest
-//     operand magnitude and any Inf/NaN code while decoding, and checks this
-//     at the end of a piece;
+//     needed when nothing can overflow).  It holds when no operand is Inf/NaN
+//     and no partial sum reaches the FP16 overflow threshold.  A chunk's
+//     partial sums are at most 3 sum_chunk |a_k b_k| (an RN step adds at most
+//     3x its non-negative addend), so 3 CL max|a| max|b| < 2^31 bounds them;
+//     the running sum changes only at chunk ends, where its largest magnitude
+//     is tracked (one max per output per chunk) and must stay below 2^31 --
+//     an overflow would leave it at 2^32 or more.  Each workgroup tracks the
+//     largest operand magnitude and any Inf/NaN code while decoding, and
+//     checks both at the end of a piece;
 //   * safe: values scaled by 2^96, which maps FP16 overflow onto FP32
 //     overflow, rounding on the raw bits (rn16s: v_bfe, v_add3, v_and).  A
 //     piece that fails the check is recomputed this way (chunk sums in the
@@ -206,9 +208,9 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 
     __shared__ __attribute__((aligned(16))) float As[2][BK][BM + PA];
     __shared__ __attribute__((aligned(16))) float Bs[2][BK][BN + PB];
-    // |a| max bits, |b| max bits, specials of the guarded pieces, in two slots
-    // used by alternate pieces
-    __shared__ uint32_t s_track[2][3];
+    // |a| max bits, |b| max bits, specials, |S| max bits of the guarded
+    // pieces, in two slots used by alternate pieces
+    __shared__ uint32_t s_track[2][4];
 
     const int tid = threadIdx.x;
     const int ly = tid / LN, lx = tid % LN;
@@ -257,6 +259,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         int chunk = c0;
         float amax_a = 0.0f, amax_b = 0.0f;  // largest magnitudes decoded
         uint32_t special = 0;                // Inf/NaN codes seen
+        float smax = 0.0f;                   // largest running sum at a chunk end
 
         auto rnd = [&](float x) __attribute__((always_inline)) -> float {
             return SAFE ? rn16s(x) : rn16v(x);
@@ -311,6 +314,13 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
                     for (int j = 0; j < TN; ++j) S[i][j] = rnd(S[i][j] + chunk_value(P[i][j]));
+                if (TRACK) {
+#pragma unroll
+                    for (int i = 0; i < TM; ++i)
+#pragma unroll
+                        for (int j = 0; j < TN; j += 2)
+                            smax = max3_abs(smax, S[i][j], S[i][TN > 1 ? j + 1 : j]);
+                }
             }
             ++chunk;                     // the next chunk starts with first_step
         };
@@ -385,38 +395,46 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         if (crem != g.CL) flush();       // the last, shorter chunk
 
         if (!SAFE) {
-            // Largest magnitudes over the workgroup's operands of this piece
-            // (reduced within each wave, then one LDS atomic per wave).  The
-            // bound uses the full K, so that pieces of one tile that each pass
-            // bound the whole chain together.  Slot `gslot` was cleared during
-            // the previous guarded piece and is read after the one barrier
-            // here; the other slot, cleared now, is next written after at
-            // least one more barrier (every piece has a slab).
+            // Largest magnitudes over the workgroup's operands and running
+            // sums of this piece (reduced within each wave, then one LDS
+            // atomic per wave).  A piece that leaves chunk sums in the
+            // workspace computes no running sum (the fold pass adds them in
+            // the scaled domain, where overflow is exact); the first piece of
+            // a shared tile and whole tiles are checked on their running sums.
+            // Slot `gslot` was cleared during the previous guarded piece and
+            // is read after the one barrier here; the other slot, cleared
+            // now, is next written after at least one more barrier (every
+            // piece has a slab).
             uint32_t* st = s_track[gslot];
             uint32_t ua = __float_as_uint(amax_a), ub = __float_as_uint(amax_b), us = special;
+            uint32_t uS = __float_as_uint(smax);
 #pragma unroll
             for (int o = 32; o > 0; o >>= 1) {      // non-negative floats: bit order
                 ua = max(ua, (uint32_t)__shfl_xor((int)ua, o));
                 ub = max(ub, (uint32_t)__shfl_xor((int)ub, o));
                 us |= (uint32_t)__shfl_xor((int)us, o);
+                uS = max(uS, (uint32_t)__shfl_xor((int)uS, o));
             }
             if ((tid & 63) == 0) {
                 atomicMax(&st[0], ua);
                 atomicMax(&st[1], ub);
                 atomicOr(&st[2], us);
+                atomicMax(&st[3], uS);
             }
             if (tid == 0) {
-                s_track[gslot ^ 1][0] = 0;
-                s_track[gslot ^ 1][1] = 0;
-                s_track[gslot ^ 1][2] = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) s_track[gslot ^ 1][q] = 0;
             }
             __syncthreads();
             const float ma = __uint_as_float(st[0]), mb = __uint_as_float(st[1]);
             const uint32_t sp = st[2];
+            const float sm = __uint_as_float(st[3]);
             gslot ^= 1;
             if (sp) return false;                                   // Inf or NaN operand
-            const double bound = 9.0 * (double)g.K * (double)ma * (double)mb;
+            // chunk partial sums: at most 3 CL max|a| max|b| (CL <= K here)
+            const double bound = 3.0 * (double)g.CL * (double)ma * (double)mb;
             if (!(bound < 2147483648.0)) return false;             // 2^31
+            if (!(sm < 2147483648.0f)) return false;               // running sums
         }
         if (to_ws) return true;
         // The first piece of a shared tile leaves its running sum for the
@@ -432,7 +450,8 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         // The running sum: a lane's TN consecutive codes of a row are stored
         // in pairs when the whole row lies inside C and is aligned; the FP8
         // result (whole tiles only: shared tiles get it from the fold pass)
-        // byte by byte.
+        // four codes per 4-byte store under the same conditions, else byte
+        // by byte.
         const int nl = n0 + lx * TN;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
@@ -455,9 +474,23 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             }
             if (g.C8 && lt < 0) {
                 uint8_t* qrow = g.C8 + (int64_t)m * g.ldc8 + nl;
+                if (TN % 4 == 0 && g.c8_vec4 && nl + TN <= g.N) {
+                    // Q8(RN32(value * scale)): the 2^-DOM scaling is exact
+                    const float u = __builtin_ldexpf(1.0f, -DOM);
 #pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    if (nl + j < g.N) qrow[j] = (uint8_t)f32d_to_fp8_scaled<DOM>(S[i][j], g.q_scale);
+                    for (int j = 0; j < TN; j += 4) {
+                        uint32_t q = f32x2_to_fp8x2<false>((S[i][j] * u) * g.q_scale,
+                                                           (S[i][j + 1] * u) * g.q_scale, 0u);
+                        q = f32x2_to_fp8x2<true>((S[i][j + 2] * u) * g.q_scale,
+                                                 (S[i][j + 3] * u) * g.q_scale, q);
+                        reinterpret_cast<uint32_t*>(qrow)[j / 4] = q;
+                    }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        if (nl + j < g.N)
+                            qrow[j] = (uint8_t)f32d_to_fp8_scaled<DOM>(S[i][j], g.q_scale);
+                }
             }
         }
         return true;

@@ -67,13 +67,15 @@ SHAPES = [
 ]
 
 
-@pytest.mark.parametrize("plan", ["auto", "shared"])
+@pytest.mark.parametrize("plan", ["auto", "shared", "tile8x8"])
 @pytest.mark.parametrize("mode", [fp8t.EXACT, fp8t.FAST])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0)])
 def test_chunk_gemm_fp8_matches_quantized_result(ta, tb, mode, plan, monkeypatch):
     if plan == "shared":
         monkeypatch.setenv("FP8T_GEMM_SPLIT", "1")
         monkeypatch.setenv("FP8T_GEMM_WGS", "5")
+    if plan == "tile8x8":                   # 8 x 8 register tiles (exact mode)
+        monkeypatch.setenv("FP8T_VALU_TILE", "1")
     rng = np.random.default_rng(700 + 2 * ta + tb + 10 * mode)
     for (M, N, K, CL) in SHAPES:
         A, B = _operands(rng, M, N, K, ta, tb)
@@ -83,11 +85,12 @@ def test_chunk_gemm_fp8_matches_quantized_result(ta, tb, mode, plan, monkeypatch
             assert np.array_equal(C16, oracle.chunk_gemm(A, B, CL, ta, tb))
         for scale in (1.0, 1000.0, 0.125):
             ref = oracle.fp8_quantize(C16, scale)
-            for with_c in (True, False):
+            # a leading dimension that allows no wide stores, and one that
+            # allows 4- and 8-byte stores
+            for with_c, ldc8 in ((True, N + 3), (False, N + 3), (False, (N + 3) // 8 * 8 + 8)):
                 say(f"chunk_gemm_fp8 mode={mode} plan={plan} ta={ta} tb={tb} {M}x{N}x{K} "
-                    f"CL={CL} scale={scale} C={with_c}")
-                Cg, C8 = run_fp8(Ad, Bd, M, N, K, CL, ta, tb, mode, scale, with_c,
-                                 ldc8=N + 3)
+                    f"CL={CL} scale={scale} C={with_c} ldc8={ldc8}")
+                Cg, C8 = run_fp8(Ad, Bd, M, N, K, CL, ta, tb, mode, scale, with_c, ldc8=ldc8)
                 assert np.array_equal(C8, ref), np.argwhere(C8 != ref)[:5]
                 if with_c:
                     assert np.array_equal(Cg, C16)

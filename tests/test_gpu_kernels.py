@@ -184,7 +184,9 @@ def _operands(rng, M, N, K, ta, tb, scale=1.0):
     return A, B
 
 
-VALU_TILES = ["auto", "0", "1", "2", "3", "4", "5", "6", "7", "8"]
+# 0-8: register tiles of the main exact kernel; 9: the chain kernel (whole
+# 32 x 32 tiles, 4-k groups; CL = 2 falls back to the others)
+VALU_TILES = ["auto", "0", "1", "2", "3", "4", "5", "6", "7", "8", "9"]
 
 
 @pytest.mark.parametrize("guard", ["1", "0"])
@@ -456,36 +458,50 @@ def test_chunk_gemm_guard_falls_back_per_piece(monkeypatch):
     A[200, 700] = 0xFC                  # -Inf
     B[:, 3] = np.where(rng.random(K) < 0.5, 0x7A, 0xFA)   # +-49152
     Co = oracle.chunk_gemm(A, B, CL)
-    for split in ("0", "1"):
-        for wgs in ("0", "7"):
-            monkeypatch.setenv("FP8T_GEMM_SPLIT", split)
-            monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
-            say(f"guard fallback split={split} wgs={wgs}")
-            Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
-            assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
+    for tile, split, wgs in (("auto", "0", "0"), ("auto", "0", "7"), ("auto", "1", "0"),
+                             ("auto", "1", "7"), ("9", "0", "0"), ("9", "0", "7")):
+        if tile == "auto":
+            monkeypatch.delenv("FP8T_VALU_TILE", raising=False)
+        else:
+            monkeypatch.setenv("FP8T_VALU_TILE", tile)
+        monkeypatch.setenv("FP8T_GEMM_SPLIT", split)
+        monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
+        say(f"guard fallback tile={tile} split={split} wgs={wgs}")
+        Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
+        assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
 
 
-@pytest.mark.parametrize("bmax", [0x44, 0x45])
-def test_chunk_gemm_guard_threshold(bmax, monkeypatch):
-    """All-positive operands with 9 K max|a| max|b| just below 2^31
-    (max|b| = 4: 2.114e9, the guarded path) and just above (max|b| = 5:
-    2.642e9, the safe path), every tile holding the maxima; both give the
-    oracle's bits, whole-tile and shared-tile plans alike."""
-    rng = np.random.default_rng(571)
-    M, N, K, CL = 192, 200, 1024, 64
-    A = rng.integers(0, 0x7B, (M, K)).astype(np.uint8)        # positive, < 57344
-    A[:, ::97] = 0x7B                                         # 57344 in every row
-    B = rng.integers(0, bmax, (K, N)).astype(np.uint8)
-    B[0, :] = bmax                                            # 4.0 or 5.0 in every column
-    bound = 9 * K * 57344 * float(oracle.p8_value(np.uint8(bmax)))
-    assert (bound < 2 ** 31) == (bmax == 0x44)
+@pytest.mark.parametrize("tile", ["auto", "4", "9", "11"])
+@pytest.mark.parametrize("CL", [64, 1024])
+@pytest.mark.parametrize("b0", [0x50, 0x52, 0x56])
+def test_chunk_gemm_guard_threshold(b0, CL, tile, monkeypatch):
+    """All-positive operands whose running sums end near the guard's 2^31:
+    A mostly 57344 and B mostly b0 = 32 (results 1.6e9 - 1.7e9: the guarded
+    path), 48 (2.3e9 - 2.5e9: the tracked running sum fails the guard, the
+    safe path) or 96 (beyond 4.29e9: FP16 overflow to Inf), with 10% smaller
+    entries; CL = 64 keeps the chunk bound 3 CL max|a| max|b| below 2^31,
+    CL = K = 1024 does not.  Every register tile and plan gives the oracle's
+    bits."""
+    if tile != "auto":
+        monkeypatch.setenv("FP8T_VALU_TILE", tile)
+    rng = np.random.default_rng(571 + b0)
+    M, N, K = 192, 200, 1024
+    A = np.full((M, K), 0x7B, np.uint8)
+    B = np.full((K, N), b0, np.uint8)
+    ma = rng.random(A.shape) < 0.1
+    A[ma] = rng.integers(0x60, 0x7B, int(ma.sum()))
+    mb = rng.random(B.shape) < 0.1
+    B[mb] = rng.integers(0x40, b0, int(mb.sum()))
     Co = oracle.chunk_gemm(A, B, CL)
+    v = oracle.p16_value(Co)
+    say(f"guard threshold b0={b0:#x} CL={CL} tile={tile}: largest result {np.max(v):.4g}")
     for split, wgs in (("0", "0"), ("1", "7")):
         for guard in ("1", "0"):
             monkeypatch.setenv("FP8T_GEMM_SPLIT", split)
             monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
             monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
-            say(f"guard threshold bmax={bmax:#x} split={split} wgs={wgs} guard={guard}")
+            say(f"guard threshold b0={b0:#x} CL={CL} tile={tile} split={split} wgs={wgs} "
+                f"guard={guard}")
             Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
             assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
 

@@ -4,8 +4,10 @@ nearest after every addition).
 
 The guarded kernels add FP8 products in plain FP32 registers and round with
 Veltkamp splitting, which is only right while no partial sum can reach FP16's
-overflow threshold.  They take the guarded path when 9 K max|a| max|b| < 2^31,
-which rests on three facts, pinned here:
+overflow threshold.  They keep a result of the guarded path when
+3 CL max|a| max|b| < 2^31 (every chunk's partial sums) and the running sums,
+tracked at chunk ends, stay below 2^31 (an overflow would leave one at 2^32 or
+more), which rests on three facts, pinned here:
 
 1. one rounded addition of a non-negative x raises a non-negative FP16 sum T
    by at most 3x: RN16(T + x) - T <= 3x, checked exhaustively over every pair
@@ -13,9 +15,9 @@ which rests on three facts, pinned here:
    program with its own integer rounding; 1.04e9 pairs);
 2. rounding is monotone and odd, so every partial sum of a chain of signed
    terms is bounded in magnitude by the same chain over the absolute values;
-   with (1) each chunk's partial sum is at most 3 sum_chunk |p| and the running
-   sum at most 3 sum_c P_c <= 9 sum_k |p_k| (checked on adversarial and random
-   chains through the oracle's addition);
+   with (1) each chunk's partial sum is at most 3 sum_chunk |p| (and the
+   running sum at most 3 sum_c P_c <= 9 sum_k |p_k|; checked on adversarial
+   and random chains through the oracle's addition);
 3. Veltkamp splitting leaves FP16 subnormal sums unchanged: every partial sum
    of FP8 products is a multiple of 2^-39, so one below 2^-30 is m 2^-39 with
    m < 512 -- exact in FP32 and already an FP16 value.
