@@ -215,7 +215,8 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
         const int kend = kend64 < g.K ? (int)kend64 : g.K;
         const bool to_ws = c0 > 0;
         int chunk = c0;
-        float vmax = 0.0f;                 // guarded: largest |p| and |S|
+        float vmax = 0.0f;                 // guarded: largest |S| at chunk ends
+        bool nonfinite = false;            // guarded: a chunk sum for the fold was not finite
 
 #pragma unroll
         for (int i = 0; i < FM; ++i)
@@ -230,20 +231,22 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < FN; ++j)
+                for (int j = 0; j < FN; ++j) {
 #pragma unroll
                     for (int r = 0; r < NR; ++r) {
-                        float s;
-                        if (SAFE) {
-                            s = rn16s(S[i][j][r] + rn16s(acc[i][j][r] * 0x1p96f));
-                        } else {
-                            const float pv = rn16v(acc[i][j][r]);
-                            s = rn16v(S[i][j][r] + pv);
-                            vmax = max3_abs(vmax, pv, s);
-                        }
-                        S[i][j][r] = s;
+                        S[i][j][r] = SAFE ? rn16s(S[i][j][r] + rn16s(acc[i][j][r] * 0x1p96f))
+                                          : rn16v(S[i][j][r] + rn16v(acc[i][j][r]));
                         acc[i][j][r] = 0.0f;
                     }
+                    // the guard: running sums at chunk ends (a chunk sum that
+                    // overflowed shows in them; v_max3 drops NaN, which the
+                    // check of the final sums catches)
+                    if (!SAFE) {
+#pragma unroll
+                        for (int r = 0; r < NR; r += 2)
+                            vmax = max3_abs(vmax, S[i][j][r], S[i][j][NR > 1 ? r + 1 : r]);
+                    }
+                }
         };
         auto flush_ws = [&](acc_t (&acc)[FM][FN]) __attribute__((always_inline)) {
 #pragma unroll
@@ -259,8 +262,9 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                         if (SAFE) {
                             pv = rn16s(acc[i][j][r] * 0x1p96f);
                         } else {
+                            // Veltkamp rounding turns an Inf sum into NaN
                             pv = rn16v(acc[i][j][r]);
-                            vmax = fmaxf(vmax, fabsf(pv));
+                            nonfinite |= !(fabsf(pv) < 2147483648.0f);
                         }
                         dst[I::out_row(lane, r) * BN] = f32d_to_fp16<DOM>(pv);
                         acc[i][j][r] = 0.0f;
@@ -368,7 +372,22 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
         __syncthreads();                   // LDS is reused by the next piece
         if (crem != g.CL) flush();         // the last, shorter chunk
 
-        if (!SAFE && __syncthreads_or(!(vmax < 4294967296.0f))) return false;   // 2^32
+        // The guard: running sums below 2^31 at every chunk end, so no chunk
+        // sum or sum reached FP16's overflow threshold (one that did would
+        // leave a running sum at 2^31 or more); and no Inf/NaN operand, whose
+        // chunk sum the guarded rounding turns into a NaN that then stays in
+        // the running sum to the end (v_max3 drops NaN: the comparison of
+        // the final sums catches it).
+        if (!SAFE) {
+            bool bad = !(vmax < 2147483648.0f) || nonfinite;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int r = 0; r < NR; ++r) bad |= !(fabsf(S[i][j][r]) < 2147483648.0f);
+            if (__syncthreads_or(bad)) return false;
+        }
         if (to_ws) return true;
         // Results leave through LDS (free after the last slab's barrier): the
         // tile's FP16 codes are staged there, then every thread writes 8

@@ -216,11 +216,6 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
             pr[r] = SAFE ? rn16s(acc[r] * 0x1p96f) : rn16v(acc[r]);
             dst[64 * r] = pr[r];
         }
-        if (!SAFE) {
-            // the guard's largest |p| (its largest |S| is taken in chain)
-#pragma unroll
-            for (int r = 0; r < 16; r += 2) vmax = max3_abs(vmax, pr[r], pr[r + 1]);
-        }
     };
 
     // The running sums of the thread's 4 outputs over the step's chunks, in
@@ -346,7 +341,14 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
             chain(std::integral_constant<bool, false>{}, cur.s);
             if (cur.s + 1 == nsteps) {
                 // tile end: the guard over the whole workgroup
-                const bool bad = __syncthreads_or(!(vmax < 4294967296.0f));   // 2^32
+                // running sums below 2^31 at every chunk end (see chain), and
+                // no Inf/NaN operand: the guarded rounding turns an Inf chunk
+                // sum into NaN, which stays in the running sum to the end and
+                // which v_max3 drops, so the final sums are compared
+                bool bad_l = !(vmax < 2147483648.0f);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) bad_l |= !(fabsf(S[i]) < 2147483648.0f);
+                const bool bad = __syncthreads_or(bad_l);
                 if (bad) {
                     if (tid == 0) {
                         if (n_redo < kRedoMax) redo[n_redo] = ordinal;

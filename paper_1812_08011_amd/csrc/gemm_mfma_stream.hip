@@ -14,10 +14,12 @@
 //     from memory while the current one is consumed, so short pieces (K of a
 //     few chunks) do not pay the memory latency once per tile;
 //   * only the guarded epilogue (plain values, Veltkamp rounding, running
-//     max of |p| and |S|) runs in the stream.  A piece in which a value
-//     reached 2^32 (FP16 overflow) is remembered and recomputed after the
-//     stream with the 2^96-scaled epilogue (integer rounding on raw bits),
-//     which gives the same bits wherever the guarded one is valid.
+//     max of |S| at chunk ends) runs in the stream.  A piece in which a
+//     running sum reached 2^31 (so a chunk sum or sum may have overflowed
+//     FP16) or ended NaN (Inf operands: Veltkamp rounding of Inf gives NaN,
+//     which stays) is remembered and recomputed after the stream with the
+//     2^96-scaled epilogue (integer rounding on raw bits), which gives the
+//     same bits wherever the guarded one is valid.
 // Slabs are staged in LDS k-contiguous (operands stored with the row index
 // contiguous are transposed 4 x 4 bytes in registers), double-buffered with
 // one barrier per slab.  The finished tile's FP16 codes leave through an LDS
@@ -187,7 +189,8 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
     Share<TB> sb;                  // B is k-contiguous only when transposed
     v16f acc;
     float S[16];
-    float vmax = 0.0f;
+    float vmax = 0.0f;             // guarded: largest |S| at chunk ends
+    bool nonfinite = false;        // guarded: a chunk sum for the fold was not finite
     const v16f zero = {};
 
     auto geom = [&](const Item& it, int& m0, int& n0, int& kbeg, int& kend)
@@ -220,23 +223,22 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                 if (SAFE) {
                     pv = rn16s(acc[r] * 0x1p96f);
                 } else {
+                    // Veltkamp rounding turns an Inf sum into NaN
                     pv = rn16v(acc[r]);
-                    vmax = fmaxf(vmax, fabsf(pv));
+                    nonfinite |= !(fabsf(pv) < 2147483648.0f);
                 }
                 dst[out_row(lane, r) * kB] = f32d_to_fp16<DOM>(pv);
             }
         } else {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float s;
-                if (SAFE) {
-                    s = rn16s(S[r] + rn16s(acc[r] * 0x1p96f));
-                } else {
-                    const float pv = rn16v(acc[r]);
-                    s = rn16v(S[r] + pv);
-                    vmax = max3_abs(vmax, pv, s);
-                }
-                S[r] = s;
+            for (int r = 0; r < 16; ++r)
+                S[r] = SAFE ? rn16s(S[r] + rn16s(acc[r] * 0x1p96f)) : rn16v(S[r] + rn16v(acc[r]));
+            // the guard: running sums at chunk ends (a chunk sum that
+            // overflowed shows in them; v_max3 drops NaN, which the check of
+            // the final sums catches)
+            if (!SAFE) {
+#pragma unroll
+                for (int r = 0; r < 16; r += 2) vmax = max3_abs(vmax, S[r], S[r + 1]);
             }
         }
         (void)m0;
@@ -364,7 +366,13 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
             slab(std::integral_constant<bool, false>{}, cur.it, buf, cur.ks, crem, chunk);
             if (cur.ks + kB >= cur.it.kend) {
                 // piece end: the guard over the whole workgroup
-                const bool bad = __syncthreads_or(!(vmax < 4294967296.0f));   // 2^32
+                // running sums below 2^31 at every chunk end: no chunk sum
+                // or sum reached FP16's overflow threshold; no Inf/NaN
+                // operand (its NaN stays in the running sum to the end)
+                bool bad_l = !(vmax < 2147483648.0f) || nonfinite;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) bad_l |= !(fabsf(S[r]) < 2147483648.0f);
+                const bool bad = __syncthreads_or(bad_l);
                 if (bad) {
                     if (tid == 0) {
                         if (n_redo < kRedoMax) redo[n_redo] = ordinal;
@@ -374,6 +382,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                     write_sums(std::integral_constant<bool, false>{}, cur.it);
                 }
                 vmax = 0.0f;
+                nonfinite = false;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) S[r] = 0.0f;
                 crem = g.CL;

@@ -313,6 +313,36 @@ def test_chunk_gemm_fast_shared_tiles(mtile, wgs, ta, tb, monkeypatch):
         assert np.array_equal(Cw, Cs), (M, N, K, CL, np.argwhere(Cw != Cs)[:5])
 
 
+@pytest.mark.parametrize("mtile,split", [("0", "0"), ("1", "0"), ("2", "0"), ("3", "0"),
+                                         ("0", "1"), ("1", "1")])
+def test_chunk_gemm_fast_specials(mtile, split, monkeypatch):
+    """Inf and NaN operands through every matrix-core kernel, in whole tiles
+    and in the later pieces of shared tiles (chunk sums through the
+    workspace): the guarded epilogue's rounding turns an Inf chunk sum into
+    NaN, so its guard must catch it and the safe epilogue give Inf -- the
+    same bits as an all-safe run, inside the oracle's bounds."""
+    monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
+    rng = np.random.default_rng(585)
+    M, N, K, CL = 130, 67, 1000, 64
+    A, B = _operands(rng, M, N, K, 0, 0)
+    A[5, 900] = 0x7C            # +Inf in chunk 14
+    A[60, 500] = 0x7F           # NaN in chunk 7
+    B[950, 3] = 0xFC            # -Inf in chunk 14
+    A[77, 640] = 0x7C           # +Inf meeting zero and finite partners
+    Ad, Bd = dev(A), dev(B)
+    got = {}
+    for guard in ("1", "0"):
+        monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+        monkeypatch.setenv("FP8T_GEMM_SPLIT", split)
+        monkeypatch.setenv("FP8T_GEMM_WGS", "7" if split == "1" else "0")
+        say(f"fast specials mtile={mtile} split={split} guard={guard}")
+        got[guard] = host(gemm(Ad, Bd, M, N, K, CL, mode=fp8t.FAST))
+    assert np.array_equal(got["1"], got["0"]), np.argwhere(got["1"] != got["0"])[:5]
+    Co = oracle.chunk_gemm(A, B, CL, mode=oracle.FAST)
+    assert np.any((Co & 0x7FFF) == 0x7E00) and np.any(Co == 0x7F00)
+    check_fast(got["1"], A, B, CL, 0, 0, f"fast specials mtile={mtile} split={split}", Co=Co)
+
+
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_chunk_gemm_fast_chunks_over_waves_same_bits(ta, tb, monkeypatch):
     """The kernel that spreads a step's four chunks over the waves of a
