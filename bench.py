@@ -46,19 +46,20 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # HBM traffic of the exact-mode chunk_gemm calls of one step, from two
 # rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) over this benchmark,
 # calibrated by the counters of a plain device copy of known size (fetch x2.0,
-# write x1.0); average calibrated bytes per call (forward 195.0 MB,
-# backward-data 294.4 MB, weight-gradient 2402.4 MB including the chunk sums
+# write x1.0); average calibrated bytes per call (forward 189.9 MB,
+# backward-data 300.0 MB, weight-gradient 2402.6 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "bd246e28d5834368b36295bf6d6edd6b7337afd266700602de80dc55bd36a07c"
-EXACT_TRAFFIC_BYTES_PER_CALL = 964.0e6
+TRAFFIC_SOURCES_SHA256 = "79061d69458555e3464201610375fbab4292ca5ebef98c1c31d9ba613dbac90a"
+EXACT_TRAFFIC_BYTES_PER_CALL = 964.2e6
 
 
 # The sources that decide what an exact-mode chunk_gemm call runs: the VALU
 # kernel, its instantiations, the planner and fold pass, the shared device code.
 EXACT_KERNEL_SOURCES = ("chunk_gemm.hip", "fp8t_device.h", "fp8t_host.h", "gemm_plan.h",
-                        "gemm_valu.h", "gemm_valu.hip", "gemm_valu_impl.h", "gemm_valu_nn.hip",
-                        "gemm_valu_nt.hip", "gemm_valu_tn.hip", "gemm_valu_tt.hip")
+                        "gemm_chain.hip", "gemm_valu.h", "gemm_valu.hip", "gemm_valu_impl.h",
+                        "gemm_valu_nn.hip", "gemm_valu_nt.hip", "gemm_valu_tn.hip",
+                        "gemm_valu_tt.hip")
 
 
 def kernel_sources_sha256():
