@@ -198,6 +198,11 @@ double valu_ops_per_mac(int cfg) {
 // runs at a quarter of the rate a 1 x 1 tile reaches at four).
 double valu_efficiency(double w) { return w >= 4.0 ? 1.0 : w / 4.0; }
 
+// Extra VALU instructions per multiply-accumulate with FP16 operands: the
+// product's multiplication and its rounding to FP16 (and, max, add and the
+// magic-number add and subtract) replace the FMA's one.
+constexpr double kP16ProductOps = 6.0;
+
 // Matrix-core fast mode, CU time of one output-chunk (the VALU epilogue
 // dominates; the matrix-core share grows with CL) and of the per-tile start
 // (pipeline fill, C stores), measured on the conv-stage GEMMs: 64 x 64 tiles
@@ -213,7 +218,8 @@ double mfma_cost_per_tile(int cfg) {
     return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.67e-6 : 0.93e-6;
 }
 
-enum Kind { VALU_EXACT = 0, VALU_FAST = 1, MFMA_FAST = 2 };
+// VALU_P16: FP16 operands, products rounded to FP16 (chunk_gemm_p16)
+enum Kind { VALU_EXACT = 0, VALU_FAST = 1, MFMA_FAST = 2, VALU_P16 = 3 };
 
 struct Choice {
     int cfg = -1;
@@ -236,7 +242,8 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
     const int cus = device_cus();
     if (cus <= 0) return best;
     const bool mf = kind == MFMA_FAST;
-    const int fast = kind != VALU_EXACT;
+    const bool p16 = kind == VALU_P16;
+    const int fast = kind == VALU_FAST || kind == MFMA_FAST;
     const int ncfg = mf ? kMfmaConfigs : kValuConfigs;
     // Overrides for tests and tuning: the tile configuration, a cap on the
     // workgroups, and 1 / 0 to require / forbid shared tiles.
@@ -264,12 +271,16 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 t_tile = mfma_cost_per_tile(cfg);
             } else {
                 // the chain kernel: exact mode, 4-k groups inside one chunk
-                if (is_chain(cfg) && (fast || conv || (CL % 4 != 0 && CL < K))) continue;
+                if (is_chain(cfg) && (fast || conv || p16 || (CL % 4 != 0 && CL < K))) continue;
                 const ValuShape sh = valu_shape(cfg);
-                fn = conv ? valu_conv_kernel(cfg, ta) : valu_kernel(cfg, ta, tb, fast);
+                fn = conv ? valu_conv_kernel(cfg, ta)
+                   : p16  ? valu_p16_kernel(cfg, ta, tb)
+                          : valu_kernel(cfg, ta, tb, fast);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
-                // the MACs of a chunk, and its end (an add and a rounding)
-                t_out = ((double)CL * valu_ops_per_mac(cfg) + 4.0) / (kLanesPerCU * kClockHz);
+                // the MACs of a chunk, and its end (an add and a rounding); an
+                // FP16 product costs its multiplication and rounding on top
+                const double ops = valu_ops_per_mac(cfg) + (p16 ? kP16ProductOps : 0.0);
+                t_out = ((double)CL * ops + 4.0) / (kLanesPerCU * kClockHz);
             }
             if (!fn) continue;
             int occ = kernel_occupancy(fn, NT);
@@ -438,19 +449,20 @@ size_t plan_workspace(const Choice& ch, bool fp8out) {
 }
 
 size_t workspace_query(int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL, int mode,
-                       bool fp8out) {
+                       bool fp8out, bool p16 = false) {
     if (!gemm_args_ok(ta, tb, M, N, K, CL, mode)) return 0;
     if (M == 0 || N == 0 || K == 0) return 0;
     normalize_chunking(mode, K, CL);
     const int64_t cl = CL > K ? K : CL;
-    return plan_workspace(plan_gemm(kind_of(mode, K, cl), ta, tb, M, N, K, cl, true), fp8out);
+    const Kind kind = p16 ? VALU_P16 : kind_of(mode, K, cl);
+    return plan_workspace(plan_gemm(kind, ta, tb, M, N, K, cl, true), fp8out);
 }
 
 int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t CL,
               const uint8_t* A, int64_t lda, const uint8_t* B, int64_t ldb, uint16_t* C,
               int64_t ldc, uint8_t* C8, int64_t ldc8, float scale, int mode, void* workspace,
               size_t workspace_bytes, hipStream_t stream, bool fp8out,
-              bool use_scratch = false) {
+              bool use_scratch = false, bool p16 = false) {
     if (!gemm_args_ok(trans_a, trans_b, M, N, K, CL, mode)) return FP8T_EINVAL;
     if (M == 0 || N == 0) return FP8T_OK;
     if (!fp8out && !C) return FP8T_EINVAL;
@@ -478,8 +490,8 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     // With no workspace, the best plan that needs none; with one, the best
     // plan overall, which must then fit; with the scratch, the best plan that
     // fits in it.
-    const Choice ch = plan_gemm(kind_of(mode, K, cl), trans_a, trans_b, M, N, K, cl,
-                                workspace_bytes > 0, false,
+    const Kind kind = p16 ? VALU_P16 : kind_of(mode, K, cl);
+    const Choice ch = plan_gemm(kind, trans_a, trans_b, M, N, K, cl, workspace_bytes > 0, false,
                                 use_scratch ? workspace_bytes : SIZE_MAX);
     if (ch.cfg < 0) return FP8T_EHIP;
     if (plan_workspace(ch, fp8out) > workspace_bytes) return FP8T_EWORKSPACE;
@@ -504,12 +516,14 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     g.N = n;
     g.K = k;
     g.CL = cl;
-    // 4-byte loads need aligned rows; the matrix-core kernel's interior path
-    // also keeps per-thread offsets within a slab in 32 bits
-    g.a_vec = aligned(A, 4) && lda % 4 == 0 && lda < (1 << 24);
-    g.b_vec = aligned(B, 4) && ldb % 4 == 0 && ldb < (1 << 24);
-    g.a_vec16 = aligned(A, 16) && lda % 16 == 0;
-    g.b_vec16 = aligned(B, 16) && ldb % 16 == 0;
+    // 4-code loads (4 bytes, or 8 with FP16 codes) need aligned rows; the
+    // matrix-core kernel's interior path also keeps per-thread offsets within
+    // a slab in 32 bits
+    const int eb = p16 ? 2 : 1;            // bytes per operand element
+    g.a_vec = aligned(A, 4 * eb) && lda % 4 == 0 && lda < (1 << 24);
+    g.b_vec = aligned(B, 4 * eb) && ldb % 4 == 0 && ldb < (1 << 24);
+    g.a_vec16 = !p16 && aligned(A, 16) && lda % 16 == 0;
+    g.b_vec16 = !p16 && aligned(B, 16) && ldb % 16 == 0;
     g.c_vec = C && aligned(C, 4) && ldc % 2 == 0;
     g.c_vec16 = C && aligned(C, 16) && ldc % 8 == 0;
     g.c8_vec8 = C8 && aligned(C8, 8) && ldc8 % 8 == 0;
@@ -539,6 +553,20 @@ extern "C" int chunk_gemm_noalloc(int trans_a, int trans_b, int64_t M, int64_t N
                                   hipStream_t stream) {
     return gemm_call(trans_a, trans_b, M, N, K, CL, A, lda, B, ldb, C, ldc, nullptr, 0, 1.0f,
                      mode, nullptr, 0, stream, false, true);
+}
+
+extern "C" size_t chunk_gemm_p16_workspace_size(int trans_a, int trans_b, int64_t M, int64_t N,
+                                                int64_t K, int64_t CL) {
+    return workspace_query(trans_a, trans_b, M, N, K, CL, FP8T_EXACT, false, true);
+}
+
+extern "C" int chunk_gemm_p16(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K,
+                              int64_t CL, const uint16_t* A, int64_t lda, const uint16_t* B,
+                              int64_t ldb, uint16_t* C, int64_t ldc, void* workspace,
+                              size_t workspace_bytes, hipStream_t stream) {
+    return gemm_call(trans_a, trans_b, M, N, K, CL, reinterpret_cast<const uint8_t*>(A), lda,
+                     reinterpret_cast<const uint8_t*>(B), ldb, C, ldc, nullptr, 0, 1.0f,
+                     FP8T_EXACT, workspace, workspace_bytes, stream, false, false, true);
 }
 
 extern "C" size_t chunk_gemm_fp8_workspace_size(int trans_a, int trans_b, int64_t M,

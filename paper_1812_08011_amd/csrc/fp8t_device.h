@@ -53,33 +53,30 @@ __device__ __forceinline__ float fp8_to_f32(uint32_t c) {
     return __uint_as_float(bits | ((c & 0x80u) << 24));
 }
 
-// FP16 code -> plain float (exact; every FP16 value is an FP32 value).
-__device__ __forceinline__ float fp16_to_f32(uint32_t c) {
-    uint32_t e = (c >> 9) & 63u, m = c & 511u;
+// FP16 code -> value times 2^S (exact): a normal code's exponent and
+// significand go into the FP32 fields (an FP16 value 2^(e-31) (1 + m/512)
+// has FP32 exponent field e + 96 + S), a subnormal's significand m is
+// converted and scaled (m 2^-39), Inf/NaN map to Inf/NaN.  S = 0 gives the
+// plain value (every FP16 value is an FP32 value), S = 96 the scaled domain.
+template <int S>
+__device__ __forceinline__ float fp16_to_f32_pow2(uint32_t c) {
+    const uint32_t e = (c >> 9) & 63u, m = c & 511u;
     uint32_t bits;
     if (e == 63u) {
         bits = m ? kF32NaN : kF32Inf;
     } else if (e == 0u) {
-        bits = __float_as_uint((float)m * 0x1p-39f);
+        bits = __float_as_uint((float)m * __builtin_ldexpf(1.0f, S - 39));
     } else {
-        bits = ((c & 0x7FFFu) << 14) + (96u << 23);
+        bits = ((c & 0x7FFFu) << 14) + ((uint32_t)(96 + S) << 23);
     }
     return __uint_as_float(bits | ((c & 0x8000u) << 16));
 }
 
-// FP16 code -> scaled-domain float (value * 2^96, exact).
-__device__ __forceinline__ float fp16_to_f32s(uint32_t c) {
-    uint32_t e = (c >> 9) & 63u, m = c & 511u;
-    uint32_t bits;
-    if (e == 63u) {
-        bits = m ? kF32NaN : kF32Inf;
-    } else if (e == 0u) {
-        bits = __float_as_uint((float)m * 0x1p57f);
-    } else {
-        bits = ((c & 0x7FFFu) << 14) + (192u << 23);
-    }
-    return __uint_as_float(bits | ((c & 0x8000u) << 16));
-}
+// FP16 code -> plain float.
+__device__ __forceinline__ float fp16_to_f32(uint32_t c) { return fp16_to_f32_pow2<0>(c); }
+
+// FP16 code -> scaled-domain float (value * 2^96).
+__device__ __forceinline__ float fp16_to_f32s(uint32_t c) { return fp16_to_f32_pow2<96>(c); }
 
 // Scaled-domain float already on the FP16 grid (low 14 bits zero) -> code.
 __device__ __forceinline__ uint16_t f32s_to_fp16(float x) {
@@ -119,6 +116,34 @@ __device__ __forceinline__ float rn16v(float x) {
     const float c = x * 16385.0f;
     const float d = c - x;
     return c - d;
+}
+
+// A product of two FP16 values rounded to FP16, nearest even (Sec. 2.3 /
+// Fig. 3(a) with FP16 multiplication).  The exact product has at most 20
+// significant bits, so the float product p is exact.  Plain values: adding
+// 1.5 x 2^(E + 14), E the exponent of p clamped below at -30, puts the last
+// kept bit of p at float's last bit (10 significant bits, or the fixed step
+// 2^-39 of FP16's subnormal range below 2^-30), and subtracting it again is
+// exact.  Valid for |p| < 2^100.
+__device__ __forceinline__ float rn16_product(float p) {
+    uint32_t e = __float_as_uint(p) & 0x7F800000u;
+    e = e > (97u << 23) ? e : (97u << 23);
+    const float magic = __uint_as_float(e + (14u << 23) + 0x00400000u);
+    return (p + magic) - magic;
+}
+
+// The same for a product held scaled by 2^64 (operands scaled by 2^48 and
+// 2^16), returned in the 2^96 domain.  The exponent that sets the magic
+// number is clamped to [34, 113]: 34 is FP16's 2^-30 there, and a product
+// above 2^113 (2^49 unscaled) overflows FP16 anyway -- the clamp only keeps
+// the magic number finite.  Zero, Inf and NaN pass through, and FP16
+// overflow becomes FP32 overflow in the final exact scaling by 2^32.
+// Compare-free: a select per product would hold a lane mask per output.
+__device__ __forceinline__ float rn16_product_s(float p) {
+    uint32_t e = __float_as_uint(p) & 0x7F800000u;
+    e = min(max(e, 161u << 23), 240u << 23);
+    const float magic = __uint_as_float(e + (14u << 23) + 0x00400000u);
+    return ((p + magic) - magic) * 0x1p32f;
 }
 
 // max(m, |a|, |b|) in one instruction (the compiler splits the fmaxf form

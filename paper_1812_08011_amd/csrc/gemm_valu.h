@@ -29,6 +29,10 @@ ValuShape valu_shape(int cfg);
 // for chunk lengths the matrix cores cannot split).
 const void* valu_kernel(int cfg, int ta, int tb, int fast);
 
+// Kernel of configuration cfg with FP16 operands (chunk_gemm_p16: products
+// rounded to FP16, exact mode); null where not built (configurations 4-8).
+const void* valu_p16_kernel(int cfg, int ta, int tb);
+
 // Exact-mode kernel of configuration cfg whose A operand is an implicitly
 // lowered convolution input (GemmArgs::conv); trans_b = 0; null where not
 // built (only configuration 4).

@@ -7,6 +7,8 @@ const void* valu_kernel_nn(int cfg, int fast);
 const void* valu_kernel_nt(int cfg, int fast);
 const void* valu_kernel_tn(int cfg, int fast);
 const void* valu_kernel_tt(int cfg, int fast);
+const void* valu_p16_kernel_n(int cfg, int tb);
+const void* valu_p16_kernel_t(int cfg, int tb);
 
 ValuShape valu_shape(int cfg) {
     switch (cfg) {
@@ -32,6 +34,11 @@ const void* valu_kernel(int cfg, int ta, int tb, int fast) {
     if (!ta && tb) return valu_kernel_nt(cfg, fast);
     if (ta && !tb) return valu_kernel_tn(cfg, fast);
     return valu_kernel_tt(cfg, fast);
+}
+
+const void* valu_p16_kernel(int cfg, int ta, int tb) {
+    if (cfg < 0 || cfg >= kValuConfigs || is_chain(cfg)) return nullptr;
+    return ta ? valu_p16_kernel_t(cfg, tb) : valu_p16_kernel_n(cfg, tb);
 }
 
 }  // namespace fp8t

@@ -183,9 +183,72 @@ __device__ __forceinline__ void slab_store(float* lds, int pitch, int tid,
     }
 }
 
+// FP16 operands (chunk_gemm_p16): the same slab layout with each thread
+// word holding 4 consecutive codes (8 bytes); `vec` allows 8-byte loads.
+template <bool KC, int R, int BK, int NT, int W>
+__device__ __forceinline__ void slab_load16(const uint16_t* __restrict__ ptr, int64_t ld,
+                                            int vec, int r0, int rows, int k0, int kend,
+                                            int tid, uint2 (&reg)[W]) {
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int d = tid + NT * w;
+        int r, k;
+        if (KC) { r = d / (BK / 4); k = (d % (BK / 4)) * 4; }
+        else    { k = d / (R / 4);  r = (d % (R / 4)) * 4; }
+        const int gr = r0 + r, gk = k0 + k;
+        uint2 v = make_uint2(0u, 0u);
+        if (gr < rows && gk < kend) {
+            const uint16_t* q = KC ? ptr + (int64_t)gr * ld + gk : ptr + (int64_t)gk * ld + gr;
+            const int lim = KC ? kend - gk : rows - gr;
+            if (vec && lim >= 4) {
+                v = *reinterpret_cast<const uint2*>(q);
+            } else {
+                uint32_t h[2] = {0u, 0u};
+                for (int b = 0; b < 4; ++b)
+                    if (b < lim) h[b / 2] |= (uint32_t)q[b] << (16 * (b % 2));
+                v = make_uint2(h[0], h[1]);
+            }
+        }
+        reg[w] = v;
+    }
+}
+
+// Decode FP16 words into the LDS slab, each value times 2^SH; TRACK keeps the
+// largest magnitude and flags Inf/NaN codes (exponent field 63: adding 0x200
+// to the masked field sets bit 15 only then).
+template <bool KC, int R, int BK, int NT, int W, int SH, bool TRACK>
+__device__ __forceinline__ void slab_store16(float* lds, int pitch, int tid,
+                                             const uint2 (&reg)[W], float& amax,
+                                             uint32_t& special) {
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        const int d = tid + NT * w;
+        const uint32_t v[2] = {reg[w].x, reg[w].y};
+        float f[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) f[b] = fp16_to_f32_pow2<SH>((v[b / 2] >> (16 * (b % 2))) & 0xFFFFu);
+        if (TRACK) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                special |= ((v[h] & 0x7E007E00u) + 0x02000200u) & 0x80008000u;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) amax = fmaxf(amax, fabsf(f[b]));
+        }
+        if (KC) {
+            const int r = d / (BK / 4), k = (d % (BK / 4)) * 4;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) lds[(k + b) * pitch + r] = f[b];
+        } else {
+            const int k = d / (R / 4), r = (d % (R / 4)) * 4;
+            *reinterpret_cast<float4*>(&lds[k * pitch + r]) = make_float4(f[0], f[1], f[2], f[3]);
+        }
+    }
+}
+
 // CONV: the A operand is the implicit lowering of an NHWC input (g.conv).
+// P16: A and B hold FP16 codes (chunk_gemm_p16, exact mode only).
 template <int TM, int TN, int LM, int LN, int BK, bool PF, int WPE, bool TA, bool TB, bool FAST,
-          bool CONV = false>
+          bool CONV = false, bool P16 = false>
 __global__ __launch_bounds__(LM * LN) __attribute__((amdgpu_waves_per_eu(WPE)))
 void chunk_gemm_valu(GemmArgs g, Plan p) {
     constexpr int NT = LM * LN;
@@ -215,16 +278,28 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
     const int tid = threadIdx.x;
     const int ly = tid / LN, lx = tid % LN;
 
-    uint32_t ra[WA], rb[WB];
+    // a thread word: 4 FP8 codes (4 bytes) or 4 FP16 codes (8 bytes)
+    typedef typename std::conditional<P16, uint2, uint32_t>::type Word;
+    Word ra[WA], rb[WB];
     float P[TM][TN], S[TM][TN];
     int gslot = 0;
     if (tid < 6) (&s_track[0][0])[tid] = 0;    // ordered by the first slab's barrier
 
     auto load_a = [&](int m0, int k0, int kend) __attribute__((always_inline)) {
-        if (CONV)
+        if constexpr (P16)
+            slab_load16<KCA, BM, BK, NT, WA>(reinterpret_cast<const uint16_t*>(g.A), g.lda,
+                                             g.a_vec, m0, g.M, k0, kend, tid, ra);
+        else if constexpr (CONV)
             slab_load_conv<KCA, BM, BK, NT, WA>(g.A, g.conv, m0, g.M, k0, kend, tid, ra);
         else
             slab_load<KCA, BM, BK, NT, WA>(g.A, g.lda, g.a_vec, m0, g.M, k0, kend, tid, ra);
+    };
+    auto load_b = [&](int n0, int k0, int kend) __attribute__((always_inline)) {
+        if constexpr (P16)
+            slab_load16<KCB, BN, BK, NT, WB>(reinterpret_cast<const uint16_t*>(g.B), g.ldb,
+                                             g.b_vec, n0, g.N, k0, kend, tid, rb);
+        else
+            slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, k0, kend, tid, rb);
     };
 
     auto lds_read = [&](float (&a)[TM], float (&b)[TN], int buf, int kk) __attribute__((always_inline)) {
@@ -267,20 +342,46 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         auto chunk_value = [&](float x) __attribute__((always_inline)) -> float {
             return FAST ? rn16s(x * 0x1p96f) : x;
         };
+        // FP16 operands: each product is rounded to FP16 before it is added
+        auto prod16 = [&](float a, float b) __attribute__((always_inline)) -> float {
+            return SAFE ? rn16_product_s(a * b) : rn16_product(a * b);
+        };
         auto first_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) P[i][j] = __builtin_fmaf(a[i], b[j], 0.0f);
+                for (int j = 0; j < TN; ++j)
+                    P[i][j] = P16 ? prod16(a[i], b[j]) + 0.0f : __builtin_fmaf(a[i], b[j], 0.0f);
         };
         auto fma_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
-                    float t = __builtin_fmaf(a[i], b[j], P[i][j]);
+                    float t = P16 ? P[i][j] + prod16(a[i], b[j])
+                                  : __builtin_fmaf(a[i], b[j], P[i][j]);
                     P[i][j] = FAST ? t : rnd(t);
                 }
+        };
+        // operand slabs: HBM -> registers, registers -> LDS (decoded; on the
+        // safe path FP8 A is scaled by 2^96, FP16 A and B by 2^48 and 2^16,
+        // their products then by 2^64)
+        auto fetch_slab = [&](int k0) __attribute__((always_inline)) {
+            load_a(m0, k0, kend);
+            load_b(n0, k0, kend);
+        };
+        auto stage_slab = [&](int buf) __attribute__((always_inline)) {
+            if constexpr (P16) {
+                slab_store16<KCA, BM, BK, NT, WA, SAFE ? 48 : 0, TRACK>(&As[buf][0][0], BM + PA,
+                                                                        tid, ra, amax_a, special);
+                slab_store16<KCB, BN, BK, NT, WB, SAFE ? 16 : 0, TRACK>(&Bs[buf][0][0], BN + PB,
+                                                                        tid, rb, amax_b, special);
+            } else {
+                slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[buf][0][0], BM + PA, tid, ra,
+                                                               amax_a, special);
+                slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[buf][0][0], BN + PB, tid, rb,
+                                                          amax_b, special);
+            }
         };
 
 #pragma unroll
@@ -328,18 +429,13 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         const int nk = kend - kbeg;
         const int nslabs = (nk + BK - 1) / BK;
         int crem = g.CL;                 // products left in the current chunk
-        load_a(m0, kbeg, kend);
-        slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, kbeg, kend, tid, rb);
-        slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[0][0][0], BM + PA, tid, ra, amax_a, special);
-        slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[0][0][0], BN + PB, tid, rb, amax_b, special);
+        fetch_slab(kbeg);
+        stage_slab(0);
         __syncthreads();
         for (int s = 0; s < nslabs; ++s) {
             const int buf = s & 1;
             const int ks = kbeg + s * BK;
-            if (s + 1 < nslabs) {
-                load_a(m0, ks + BK, kend);
-                slab_load<KCB, BN, BK, NT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, ks + BK, kend, tid, rb);
-            }
+            if (s + 1 < nslabs) fetch_slab(ks + BK);
             const int kmax = min(BK, kend - ks);
             int kk = 0;
             while (kk < kmax) {
@@ -386,10 +482,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                     crem = g.CL;
                 }
             }
-            if (s + 1 < nslabs) {
-                slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[buf ^ 1][0][0], BM + PA, tid, ra, amax_a, special);
-                slab_store<KCB, BN, BK, NT, WB, 0, TRACK>(&Bs[buf ^ 1][0][0], BN + PB, tid, rb, amax_b, special);
-            }
+            if (s + 1 < nslabs) stage_slab(buf ^ 1);
             __syncthreads();
         }
         if (crem != g.CL) flush();       // the last, shorter chunk
@@ -431,8 +524,11 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             const float sm = __uint_as_float(st[3]);
             gslot ^= 1;
             if (sp) return false;                                   // Inf or NaN operand
-            // chunk partial sums: at most 3 CL max|a| max|b| (CL <= K here)
-            const double bound = 3.0 * (double)g.CL * (double)ma * (double)mb;
+            // chunk partial sums: at most 3 CL max|a| max|b| (CL <= K here);
+            // a product rounded to FP16 is at most (1 + 2^-10) |a b|, or 2^-39
+            // in the subnormal range
+            const double bound = P16 ? 3.01 * (double)g.CL * (double)ma * (double)mb + 1.0
+                                     : 3.0 * (double)g.CL * (double)ma * (double)mb;
             if (!(bound < 2147483648.0)) return false;             // 2^31
             if (!(sm < 2147483648.0f)) return false;               // running sums
         }
@@ -576,6 +672,28 @@ const void* kernel_table(int cfg, int fast) {
         case 6: return kernel_of<6, TA, TB, false>();
         case 7: return kernel_of<7, TA, TB, false>();
         case 8: return kernel_of<8, TA, TB, false>();
+        default: return nullptr;
+    }
+}
+
+// FP16-operand kernels (chunk_gemm_p16) of the configurations built for them:
+// the 4 x 4 tiles (4, 7, 8) and the small ones for few outputs (5, 6).
+template <int C, bool TA, bool TB>
+const void* kernel_of_p16() {
+    using Q = ValuCfg<C>;
+    return reinterpret_cast<const void*>(&chunk_gemm_valu<Q::TM, Q::TN, Q::LM, Q::LN, Q::BK,
+                                                          Q::PF, Q::WPE, TA, TB, false, false,
+                                                          true>);
+}
+
+template <bool TA, bool TB>
+const void* kernel_table_p16(int cfg) {
+    switch (cfg) {
+        case 4: return kernel_of_p16<4, TA, TB>();
+        case 5: return kernel_of_p16<5, TA, TB>();
+        case 6: return kernel_of_p16<6, TA, TB>();
+        case 7: return kernel_of_p16<7, TA, TB>();
+        case 8: return kernel_of_p16<8, TA, TB>();
         default: return nullptr;
     }
 }
