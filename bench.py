@@ -99,6 +99,15 @@ def sr_gemm_peak_mac_s():
     return VALU_LANE_OPS / 12.5
 
 
+def p16_peak_mac_s(cl):
+    """ALU ceiling of chunk_gemm_p16 (FP16 operands): per multiply-accumulate
+    the product's Veltkamp rounding to FP16 (a multiply by the pre-split
+    operand, an FMA and an add), the add into the chunk sum and its rounding
+    (multiply, subtract, subtract): 7 VALU ops, plus the chunk end's 4 per
+    output.  Priced at the chip's full VALU rate."""
+    return VALU_LANE_OPS / (7.0 + 4.0 / cl)
+
+
 def parse():
     p = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     p.add_argument("--gpus", type=int, default=1)
@@ -411,6 +420,35 @@ def speech_layers_measurement(torch, fp8t):
     return res
 
 
+def p16_last_layer_measurement(torch, fp8t):
+    """chunk_gemm_p16 on the speech DNN's last layer (1024 -> 6000, batch
+    256, FP16 operands as Sec. 3 keeps them): Forward, Backward (trans_b) and
+    Gradient (trans_a) GEMMs, CL 64, each with its workspace."""
+    import workloads
+    d = workloads.speech_layer(5)
+
+    def q16(x):
+        t = torch.empty(x.shape, dtype=torch.uint16, device="cuda")
+        fp8t.fp16_quantize(torch.from_numpy(x).cuda(), t)
+        return t
+    X16, W16, E16 = q16(d["X"]), q16(d["W"]), q16(d["E"] * np.float32(d["e_scale"]))
+    res = {}
+    B, (fi, fo) = d["X"].shape[0], workloads.SPEECH_LAYERS[5]
+    for g, (A, Bm, M, N, K, ta, tb) in (("fwd", (X16, W16, B, fo, fi, 0, 0)),
+                                       ("dgrad", (E16, W16, B, fi, fo, 0, 1)),
+                                       ("wgrad", (X16, E16, fi, fo, B, 1, 0))):
+        wb = fp8t.chunk_gemm_p16_workspace_size(ta, tb, M, N, K, CL)
+        ws = torch.empty(wb, dtype=torch.uint8, device="cuda") if wb else None
+        C = torch.empty((M, N), dtype=torch.uint16, device="cuda")
+        ms = time_ms(torch, lambda: fp8t.chunk_gemm_p16(ta, tb, M, N, K, CL, A, A.shape[1], Bm,
+                                                       Bm.shape[1], C, N, ws, wb), 20)
+        rate = M * N * K / (ms * 1e-3)
+        res[f"{M}x{N}x{K}_{g}"] = {"ms": ms, "tmac_s": rate / 1e12,
+                                   "frac_of_alu_bound": rate / p16_peak_mac_s(CL),
+                                   "workspace_mb": wb / 1e6}
+    return res
+
+
 def cpu_baseline_configs(target_s=2.0):
     """The oracle timed beside the other configurations (all host cores, a
     bounded sample each): the small GEMM and update in full, and sampled
@@ -658,6 +696,7 @@ def main():
         result["kernels"]["small"] = small_measurement(torch, fp8t)
         result["kernels"]["sweep"] = sweep_measurement(torch, fp8t)
         result["kernels"]["speech_layers"] = speech_layers_measurement(torch, fp8t)
+        result["kernels"]["p16_last_layer"] = p16_last_layer_measurement(torch, fp8t)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(work, args.cpu_seconds)
         if not args.no_extras:

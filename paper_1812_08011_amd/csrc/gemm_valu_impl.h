@@ -215,11 +215,18 @@ __device__ __forceinline__ void slab_load16(const uint16_t* __restrict__ ptr, in
 
 // Decode FP16 words into the LDS slab, each value times 2^SH; TRACK keeps the
 // largest magnitude and flags Inf/NaN codes (exponent field 63: adding 0x200
-// to the masked field sets bit 15 only then).
+// to the masked field sets bit 15 only then), and lowers kmin[k] to the
+// smallest nonzero magnitude staged at k, held as its bit pattern minus one
+// (a zero wraps to ~0, which never lowers the entry).
 template <bool KC, int R, int BK, int NT, int W, int SH, bool TRACK>
 __device__ __forceinline__ void slab_store16(float* lds, int pitch, int tid,
                                              const uint2 (&reg)[W], float& amax,
-                                             uint32_t& special) {
+                                             uint32_t& special, uint32_t* kmin) {
+    static_assert(NT % (BK / 4) == 0, "a thread's words share one k group");
+    auto key = [](float f) __attribute__((always_inline)) -> uint32_t {
+        return (__float_as_uint(f) & 0x7FFFFFFFu) - 1u;
+    };
+    uint32_t mk[4] = {~0u, ~0u, ~0u, ~0u};  // KC: minima of this thread's 4 k
 #pragma unroll
     for (int w = 0; w < W; ++w) {
         const int d = tid + NT * w;
@@ -233,6 +240,13 @@ __device__ __forceinline__ void slab_store16(float* lds, int pitch, int tid,
                 special |= ((v[h] & 0x7E007E00u) + 0x02000200u) & 0x80008000u;
 #pragma unroll
             for (int b = 0; b < 4; ++b) amax = fmaxf(amax, fabsf(f[b]));
+            if (KC) {
+#pragma unroll
+                for (int b = 0; b < 4; ++b) mk[b] = min(mk[b], key(f[b]));
+            } else {
+                const int k = d / (R / 4);
+                atomicMin(&kmin[k], min(min(key(f[0]), key(f[1])), min(key(f[2]), key(f[3]))));
+            }
         }
         if (KC) {
             const int r = d / (BK / 4), k = (d % (BK / 4)) * 4;
@@ -242,6 +256,11 @@ __device__ __forceinline__ void slab_store16(float* lds, int pitch, int tid,
             const int k = d / (R / 4), r = (d % (R / 4)) * 4;
             *reinterpret_cast<float4*>(&lds[k * pitch + r]) = make_float4(f[0], f[1], f[2], f[3]);
         }
+    }
+    if (TRACK && KC) {
+        const int k = (tid % (BK / 4)) * 4;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) atomicMin(&kmin[k + b], mk[b]);
     }
 }
 
@@ -274,6 +293,10 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
     // |a| max bits, |b| max bits, specials, |S| max bits of the guarded
     // pieces, in two slots used by alternate pieces
     __shared__ uint32_t s_track[2][4];
+    // FP16 operands on the guarded path: per k of a staged slab, the smallest
+    // nonzero |a| over the tile's rows and |b| over its columns (bit pattern
+    // minus one, ~0 for none), in three slots used by successive slabs
+    __shared__ uint32_t s_kmin[P16 ? 3 : 1][2][P16 ? BK : 1];
 
     const int tid = threadIdx.x;
     const int ly = tid / LN, lx = tid % LN;
@@ -284,6 +307,14 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
     float P[TM][TN], S[TM][TN];
     int gslot = 0;
     if (tid < 6) (&s_track[0][0])[tid] = 0;    // ordered by the first slab's barrier
+    // Slabs staged on the guarded path so far; slab c fills slot c % 3 and
+    // clears slot (c + 1) % 3, whose last reader (slab c - 2) finished before
+    // the barrier that precedes the staging of slab c.
+    int sc = 0;
+    if (P16) {
+        for (int q = tid; q < 3 * 2 * BK; q += NT) (&s_kmin[0][0][0])[q] = ~0u;
+        __syncthreads();
+    }
 
     auto load_a = [&](int m0, int k0, int kend) __attribute__((always_inline)) {
         if constexpr (P16)
@@ -342,24 +373,54 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         auto chunk_value = [&](float x) __attribute__((always_inline)) -> float {
             return FAST ? rn16s(x * 0x1p96f) : x;
         };
-        // FP16 operands: each product is rounded to FP16 before it is added
-        auto prod16 = [&](float a, float b) __attribute__((always_inline)) -> float {
-            return SAFE ? rn16_product_s(a * b) : rn16_product(a * b);
-        };
-        auto first_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
+        // FP16 operands: each product is rounded to FP16 before it is added.
+        // With VSPLIT (guarded path, every nonzero product of the slab at
+        // least 2^-30) by Veltkamp splitting of the exact product p = a b:
+        // c = a (b (2^14 + 1)) is RN(p (2^14 + 1)) -- b (2^14 + 1) is exact,
+        // b having at most 10 significant bits -- and p - c = fma(a, b, -c),
+        // so hi = c + fma(a, b, -c) is rn16v(p) in three instructions (a zero
+        // product gives +0).  Otherwise by the clamped magic-number add.
+        auto first_step = [&](auto vsplit, const float (&a)[TM], const float (&b)[TN])
+                              __attribute__((always_inline)) {
+            constexpr bool VSPLIT = decltype(vsplit)::value;
+            float bs[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    P[i][j] = P16 ? prod16(a[i], b[j]) + 0.0f : __builtin_fmaf(a[i], b[j], 0.0f);
-        };
-        auto fma_step = [&](const float (&a)[TM], const float (&b)[TN]) __attribute__((always_inline)) {
+            for (int j = 0; j < TN; ++j) bs[j] = VSPLIT ? b[j] * 16385.0f : 0.0f;
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
-                    float t = P16 ? P[i][j] + prod16(a[i], b[j])
-                                  : __builtin_fmaf(a[i], b[j], P[i][j]);
+                    if (VSPLIT) {
+                        const float c = a[i] * bs[j];
+                        P[i][j] = c + __builtin_fmaf(a[i], b[j], -c);
+                    } else if (P16) {
+                        P[i][j] = (SAFE ? rn16_product_s(a[i] * b[j])
+                                        : rn16_product(a[i] * b[j])) + 0.0f;
+                    } else {
+                        P[i][j] = __builtin_fmaf(a[i], b[j], 0.0f);
+                    }
+                }
+        };
+        auto fma_step = [&](auto vsplit, const float (&a)[TM], const float (&b)[TN])
+                            __attribute__((always_inline)) {
+            constexpr bool VSPLIT = decltype(vsplit)::value;
+            float bs[TN];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bs[j] = VSPLIT ? b[j] * 16385.0f : 0.0f;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    float t;
+                    if (VSPLIT) {
+                        const float c = a[i] * bs[j];
+                        t = P[i][j] + (c + __builtin_fmaf(a[i], b[j], -c));
+                    } else if (P16) {
+                        t = P[i][j] + (SAFE ? rn16_product_s(a[i] * b[j])
+                                            : rn16_product(a[i] * b[j]));
+                    } else {
+                        t = __builtin_fmaf(a[i], b[j], P[i][j]);
+                    }
                     P[i][j] = FAST ? t : rnd(t);
                 }
         };
@@ -372,10 +433,15 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         };
         auto stage_slab = [&](int buf) __attribute__((always_inline)) {
             if constexpr (P16) {
-                slab_store16<KCA, BM, BK, NT, WA, SAFE ? 48 : 0, TRACK>(&As[buf][0][0], BM + PA,
-                                                                        tid, ra, amax_a, special);
-                slab_store16<KCB, BN, BK, NT, WB, SAFE ? 16 : 0, TRACK>(&Bs[buf][0][0], BN + PB,
-                                                                        tid, rb, amax_b, special);
+                uint32_t* km = &s_kmin[sc % 3][0][0];
+                slab_store16<KCA, BM, BK, NT, WA, SAFE ? 48 : 0, TRACK>(
+                    &As[buf][0][0], BM + PA, tid, ra, amax_a, special, km);
+                slab_store16<KCB, BN, BK, NT, WB, SAFE ? 16 : 0, TRACK>(
+                    &Bs[buf][0][0], BN + PB, tid, rb, amax_b, special, km + BK);
+                if (TRACK) {
+                    if (tid < 2 * BK) (&s_kmin[(sc + 1) % 3][0][0])[tid] = ~0u;
+                    ++sc;
+                }
             } else {
                 slab_store<KCA, BM, BK, NT, WA, ASHIFT, TRACK>(&As[buf][0][0], BM + PA, tid, ra,
                                                                amax_a, special);
@@ -429,6 +495,20 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         const int nk = kend - kbeg;
         const int nslabs = (nk + BK - 1) / BK;
         int crem = g.CL;                 // products left in the current chunk
+        const int sc0 = sc;              // guarded FP16: counter of this piece's first slab
+        // Whether every nonzero product of the staged slab in slot `slot` is
+        // at least 2^-30 (then Veltkamp splitting rounds the products): lane
+        // k of each wave checks k, and the wave votes.
+        auto slab_vsplit = [&](int slot) __attribute__((always_inline)) -> bool {
+            bool ok = true;
+            const int lane = tid & 63;
+            if (lane < BK) {
+                const uint32_t ka = s_kmin[slot][0][lane], kb = s_kmin[slot][1][lane];
+                if (ka != ~0u && kb != ~0u)
+                    ok = __uint_as_float(ka + 1u) * __uint_as_float(kb + 1u) >= 0x1p-30f;
+            }
+            return __all(ok);
+        };
         fetch_slab(kbeg);
         stage_slab(0);
         __syncthreads();
@@ -437,6 +517,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             const int ks = kbeg + s * BK;
             if (s + 1 < nslabs) fetch_slab(ks + BK);
             const int kmax = min(BK, kend - ks);
+            auto compute = [&](auto vsplit) __attribute__((always_inline)) {
             int kk = 0;
             while (kk < kmax) {
                 const int seg = min(kmax - kk, crem);
@@ -452,18 +533,18 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 #pragma unroll
                         for (int q = 0; q < BK; q += 2) {
                             lds_read(a1, b1, buf, q + 1);
-                            if (q == 0 && fresh) first_step(a0, b0);
-                            else fma_step(a0, b0);
+                            if (q == 0 && fresh) first_step(vsplit, a0, b0);
+                            else fma_step(vsplit, a0, b0);
                             if (q + 2 < BK) lds_read(a0, b0, buf, q + 2);
-                            fma_step(a1, b1);
+                            fma_step(vsplit, a1, b1);
                         }
                     } else {
 #pragma unroll
                         for (int q = 0; q < BK; ++q) {
                             float a[TM], b[TN];
                             lds_read(a, b, buf, q);
-                            if (q == 0 && fresh) first_step(a, b);
-                            else fma_step(a, b);
+                            if (q == 0 && fresh) first_step(vsplit, a, b);
+                            else fma_step(vsplit, a, b);
                         }
                     }
                 } else {
@@ -471,8 +552,8 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                     for (int q = kk; q < kk + seg; ++q) {
                         float a[TM], b[TN];
                         lds_read(a, b, buf, q);
-                        if (q == kk && fresh) first_step(a, b);
-                        else fma_step(a, b);
+                        if (q == kk && fresh) first_step(vsplit, a, b);
+                        else fma_step(vsplit, a, b);
                     }
                 }
                 kk += seg;
@@ -481,6 +562,13 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                     flush();
                     crem = g.CL;
                 }
+            }
+            };
+            if constexpr (P16 && TRACK) {
+                if (slab_vsplit((sc0 + s) % 3)) compute(std::true_type{});
+                else compute(std::false_type{});
+            } else {
+                compute(std::false_type{});
             }
             if (s + 1 < nslabs) stage_slab(buf ^ 1);
             __syncthreads();

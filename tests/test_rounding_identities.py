@@ -39,3 +39,120 @@ def test_veltkamp_split_keeps_short_values():
         assert np.array_equal(veltkamp10(x), x)
         assert np.array_equal(veltkamp10(-x), -x)
     assert veltkamp10(np.float32([0.0]))[0] == 0.0
+
+
+# --- products of two FP16 values (the FP16-operand GEMM) -------------------
+
+def fp16_operands(exp, neg=False):
+    """Every FP16 normal value 2^exp (1 + m/512), m = 0..511, as float32."""
+    v = (512.0 + np.arange(512)) * 2.0 ** (exp - 9)
+    return (-v if neg else v).astype(np.float32)
+
+
+def rn16_reference(p):
+    """Exact products (float64) rounded to the FP16 grid by integer
+    arithmetic: quantum 2^(max(E, -30) - 9) for |p| in [2^E, 2^(E+1)), ties
+    to even; Inf from the largest FP16 value's midpoint on."""
+    p = np.asarray(p, np.float64)
+    e = np.floor(np.log2(np.where(p == 0, 1.0, np.abs(p))))
+    q = np.exp2(np.maximum(e, -30.0) - 9.0)
+    r = np.rint(p / q) * q
+    r = np.where(np.abs(r) >= 2.0 ** 32, np.inf * np.sign(p), r)
+    return np.where(p == 0, 0.0, r)
+
+
+def fma32(a, b, c):
+    """fmaf(a, b, c) for float32 a, b, c when a b is exact in float64 and
+    a b + c needs at most 53 bits: one rounding of the float64 result."""
+    return (a.astype(np.float64) * b.astype(np.float64) + c.astype(np.float64)).astype(np.float32)
+
+
+def test_fp16_product_veltkamp_split_is_rn16():
+    """c = a (b (2^14 + 1)), hi = c + fma(a, b, -c) rounds the exact product
+    of two FP16 values to FP16 (nearest even) whenever it is at least 2^-30
+    (and below the guard's 2^31): every pair of significands, both sign
+    combinations, products from 2^-30 to 2^31."""
+    for ea, eb in ((-15, -15), (-30, 0), (0, 0), (-1, -1), (15, 14), (7, -20)):
+        for na in (False, True):
+            a = fp16_operands(ea, na)[:, None]
+            b = fp16_operands(eb)[None, :]
+            bs = (b * np.float32(16385.0)).astype(np.float32)
+            assert np.array_equal(bs.astype(np.float64), b.astype(np.float64) * 16385.0)
+            c = (a * bs).astype(np.float32)
+            hi = (c + fma32(a, b, -c)).astype(np.float32)
+            exact = a.astype(np.float64) * b.astype(np.float64)
+            assert np.array_equal(hi.astype(np.float64), rn16_reference(exact)), (ea, eb, na)
+    # a zero product gives +0 whatever the signs
+    for a, b in ((0.0, 3.0), (-0.0, 3.0), (0.0, -3.0), (-2.0, 0.0)):
+        a32, b32 = np.float32([a]), np.float32([b])
+        c = (a32 * (b32 * np.float32(16385.0))).astype(np.float32)
+        hi = (c + fma32(a32, b32, -c)).astype(np.float32)
+        assert hi.view(np.uint32)[0] == 0
+
+
+def rn16_product_plain(p):
+    """The plain-value magic-number rounding of an exact float32 product."""
+    e = p.view(np.uint32) & np.uint32(0x7F800000)
+    e = np.maximum(e, np.uint32(97 << 23))
+    magic = (e + np.uint32(14 << 23) + np.uint32(0x00400000)).view(np.float32)
+    return ((p + magic).astype(np.float32) - magic).astype(np.float32)
+
+
+def rn16_product_scaled(p64):
+    """The 2^64-domain variant: clamp the exponent to [34, 113], round with
+    the magic number, return the result times 2^32 (the 2^96 domain)."""
+    e = p64.view(np.uint32) & np.uint32(0x7F800000)
+    e = np.minimum(np.maximum(e, np.uint32(161 << 23)), np.uint32(240 << 23))
+    magic = (e + np.uint32(14 << 23) + np.uint32(0x00400000)).view(np.float32)
+    with np.errstate(over="ignore", invalid="ignore"):
+        r = ((p64 + magic).astype(np.float32) - magic).astype(np.float32)
+        return (r * np.float32(2.0 ** 32)).astype(np.float32)
+
+
+def fp16_subnormals():
+    return (np.arange(1, 512) * 2.0 ** -39).astype(np.float32)
+
+
+def test_fp16_product_magic_rounding_plain():
+    """The guarded path's product rounding: every significand pair over
+    exponents that put products in FP16's subnormal range (fixed step 2^-39),
+    across the 2^-30 boundary and in the normal range; FP16 subnormal
+    operands too."""
+    cases = [(-30, -30), (-20, -12), (-16, -15), (-15, -15), (0, 0), (15, 14)]
+    for ea, eb in cases:
+        for na in (False, True):
+            a = fp16_operands(ea, na)[:, None]
+            b = fp16_operands(eb)[None, :]
+            got = rn16_product_plain((a * b).astype(np.float32))
+            exact = a.astype(np.float64) * b.astype(np.float64)
+            assert np.array_equal(got.astype(np.float64), rn16_reference(exact)), (ea, eb)
+    a = fp16_subnormals()[:, None]
+    for eb in (-10, 0, 20):
+        b = fp16_operands(eb)[None, :]
+        got = rn16_product_plain((a * b).astype(np.float32))
+        assert np.array_equal(got.astype(np.float64),
+                              rn16_reference(a.astype(np.float64) * b.astype(np.float64))), eb
+
+
+def test_fp16_product_magic_rounding_scaled():
+    """The 2^96-domain product rounding of the safe path (operands scaled by
+    2^48 and 2^16): subnormal-range, normal and overflowing products (those
+    at or beyond the largest FP16 value's midpoint become Inf), up to the
+    largest FP16 operands, and FP16 subnormal operands."""
+    cases = [(-30, -30), (-16, -15), (0, 0), (15, 15), (16, 16), (31, 31), (31, -39 + 9)]
+    for ea, eb in cases:
+        for na in (False, True):
+            a = fp16_operands(ea, na)[:, None]
+            b = fp16_operands(eb)[None, :]
+            p64 = ((a * np.float32(2.0 ** 48)) * (b * np.float32(2.0 ** 16))).astype(np.float32)
+            got = rn16_product_scaled(p64).astype(np.float64) * 2.0 ** -96
+            exact = a.astype(np.float64) * b.astype(np.float64)
+            assert np.array_equal(got, rn16_reference(exact)), (ea, eb, na)
+    a = fp16_subnormals()[:, None]
+    b = fp16_operands(-5)[None, :]
+    p64 = ((a * np.float32(2.0 ** 48)) * (b * np.float32(2.0 ** 16))).astype(np.float32)
+    got = rn16_product_scaled(p64).astype(np.float64) * 2.0 ** -96
+    assert np.array_equal(got, rn16_reference(a.astype(np.float64) * b.astype(np.float64)))
+    # zero, Inf and NaN pass through
+    z = rn16_product_scaled(np.float32([0.0, np.inf, -np.inf, np.nan]))
+    assert z[0] == 0.0 and z[1] == np.inf and z[2] == -np.inf and np.isnan(z[3])
