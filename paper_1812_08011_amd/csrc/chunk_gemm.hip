@@ -67,7 +67,9 @@ __device__ __forceinline__ float fp16_to_f32s_fold(uint32_t c) {
 // (the conv stage's weight-gradient fold is 2304 waves: 9 per CU, where
 // 256-thread workgroups left some CUs three and others two)
 constexpr int kFoldV = FP8T_FOLD_V, kFoldU = FP8T_FOLD_U, kFoldT = FP8T_FOLD_T;
-typedef std::conditional<kFoldV == 8, uint4, uint2>::type FoldVec;
+static_assert(kFoldV == 2 || kFoldV == 4 || kFoldV == 8, "2, 4 or 8 outputs per thread");
+typedef std::conditional<kFoldV == 8, uint4,
+                         std::conditional<kFoldV == 4, uint2, uint32_t>::type>::type FoldVec;
 
 __global__ __launch_bounds__(kFoldT) void chunk_fold(GemmArgs g, Plan p, int BM, int BN) {
     const int64_t per = (int64_t)BM * BN;
