@@ -53,7 +53,9 @@ __device__ __forceinline__ float fp16_to_f32s_fold(uint32_t c) {
 // load per chunk, in batches of kFoldU chunks with the next batch in flight
 // while one is added (a split GEMM has few shared outputs and many chunks, so
 // the pass needs many loads in flight per thread; 4 outputs x 16 chunks was
-// the fastest of 4/8 x 16/32 on the conv stage's weight-gradient GEMM).
+// the fastest of 4/8 x 16/32 on the conv stage's weight-gradient GEMM).  In
+// the workspace's banded layout (ws_index) the threads of a band of 4 rows
+// read one contiguous run per chunk, and its successive chunks are adjacent.
 #ifndef FP8T_FOLD_V
 #define FP8T_FOLD_V 4
 #endif
@@ -76,25 +78,28 @@ __global__ __launch_bounds__(kFoldT) void chunk_fold(GemmArgs g, Plan p, int BM,
     const int64_t idx = ((int64_t)blockIdx.x * kFoldT + threadIdx.x) * kFoldV;
     const int64_t lt = idx / per;
     if (lt * p.nch >= p.L) return;
+    // thread index -> band of 4 rows (ws_index), then row-major inside it
     const int local = (int)(idx - lt * per);
+    const int band = local / (4 * BN), pos = local % (4 * BN);
+    const int r = 4 * band + pos / BN, c = pos % BN;
     const int64_t tile = p.t_whole + lt;
     int tr, tc;
     tile_rc(p, tile, tr, tc);
-    const int m = tr * BM + local / BN;
-    const int n0 = tc * BN + local % BN;
+    const int m = tr * BM + r;
+    const int n0 = tc * BN + c;
     if (m >= g.M || n0 >= g.N) return;
     const int a = first_piece_end(p, lt);
     // a tile whose first piece took every chunk needs only its FP8 result
     if (a >= p.nch && !g.C8) return;
     // the running sum of the first piece: in C, or in s_ws (FP8 result only)
     uint16_t* cp = g.C ? g.C + (int64_t)m * g.ldc + n0 : nullptr;
-    const uint16_t* sp = g.C ? cp : g.s_ws + lt * per + local;
+    const uint16_t* sp = g.C ? cp : g.s_ws + lt * per + r * BN + c;
     const int nv = min(kFoldV, g.N - n0);
     float S[kFoldV];
 #pragma unroll
     for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fp16_to_f32s_fold(sp[v]) : 0.0f;
-    const FoldVec* src = reinterpret_cast<const FoldVec*>(g.ws + lt * p.nch * per + local);
-    const int64_t step = per / kFoldV;          // vectors per chunk
+    const FoldVec* src = reinterpret_cast<const FoldVec*>(g.ws + ws_index(p, BM, BN, lt, 0, r, c));
+    const int64_t step = 4 * BN / kFoldV;       // vectors per chunk of a band
     auto add = [&](FoldVec q) __attribute__((always_inline)) {
         uint32_t w[kFoldV / 2];
         __builtin_memcpy(w, &q, sizeof(q));

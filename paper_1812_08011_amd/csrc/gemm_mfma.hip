@@ -253,9 +253,8 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j) {
-                    uint16_t* dst = g.ws + (lt * p.nch + chunk) * (int64_t)(BM * BN) +
-                                    (wy * FM * BW + i * BW) * BN + wx * FN * BW + j * BW +
-                                    I::out_col(lane);
+                    const int r0 = wy * FM * BW + i * BW;
+                    const int c = wx * FN * BW + j * BW + I::out_col(lane);
 #pragma unroll
                     for (int r = 0; r < NR; ++r) {
                         float pv;
@@ -266,7 +265,8 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                             pv = rn16v(acc[i][j][r]);
                             nonfinite |= !(fabsf(pv) < 2147483648.0f);
                         }
-                        dst[I::out_row(lane, r) * BN] = f32d_to_fp16<DOM>(pv);
+                        g.ws[ws_index(p, BM, BN, lt, chunk, r0 + I::out_row(lane, r), c)] =
+                            f32d_to_fp16<DOM>(pv);
                         acc[i][j][r] = 0.0f;
                     }
                 }

@@ -215,8 +215,6 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
         constexpr bool SAFE = decltype(safe_tag)::value;
         constexpr int DOM = SAFE ? 96 : 0;
         if (it.c0 > 0) {
-            uint16_t* dst = g.ws + (it.lt * p.nch + chunk) * (int64_t)(kB * kB) +
-                            (wy * 32) * kB + bcol;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 float pv;
@@ -227,7 +225,8 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                     pv = rn16v(acc[r]);
                     nonfinite |= !(fabsf(pv) < 2147483648.0f);
                 }
-                dst[out_row(lane, r) * kB] = f32d_to_fp16<DOM>(pv);
+                g.ws[ws_index(p, kB, kB, it.lt, chunk, wy * 32 + out_row(lane, r), bcol)] =
+                    f32d_to_fp16<DOM>(pv);
             }
         } else {
 #pragma unroll

@@ -13,9 +13,9 @@
 //     [w * L / G, (w + 1) * L / G), so every workgroup ends with the same
 //     number of chunks.  A range piece that starts at chunk 0 of its tile
 //     writes the running sum of its chunks to C; a piece that starts later
-//     writes each chunk's FP16 sum to the workspace, and chunk_fold then
-//     continues the running sum from C over those chunk sums in ascending
-//     order.  The additions are the same ones, in the same order, as when a
+//     writes each chunk's FP16 sum to the workspace (ws_index), and
+//     chunk_fold then continues the running sum from C over those chunk sums
+//     in ascending order.  The additions are the same ones, in the same order, as when a
 //     tile is processed whole, so the result does not depend on the plan.
 #pragma once
 
@@ -94,6 +94,16 @@ __host__ __device__ inline void tile_rc(const Plan& p, int64_t tile, int& tr, in
         tr = (int)q;
         tc = (int)(tile - q * p.tiles_n);
     }
+}
+
+// Workspace index of the chunk sum of chunk `chunk` of output (r, c) of
+// shared tile lt (BM x BN tiles, BM a multiple of 4): the tile's rows in
+// bands of 4, each band's sums of one chunk a run of 4 BN codes, the runs of
+// a band in chunk order.  The fold pass, one wave per band, then reads each
+// band's successive chunks from consecutive memory.
+__host__ __device__ inline int64_t ws_index(const Plan& p, int BM, int BN, int64_t lt, int chunk,
+                                            int r, int c) {
+    return ((lt * (BM / 4) + r / 4) * p.nch + chunk) * (int64_t)(4 * BN) + (r % 4) * BN + c;
 }
 
 // First chunk of shared tile lt that the workspace holds: the end of the

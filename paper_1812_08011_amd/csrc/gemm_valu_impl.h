@@ -457,9 +457,9 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 
         auto flush = [&]() __attribute__((always_inline)) {
             if (to_ws) {
-                uint16_t* dst = g.ws + ((lt * p.nch + chunk) * BM + ly * TM) * BN + lx * TN;
 #pragma unroll
                 for (int i = 0; i < TM; ++i) {
+                    uint16_t* dst = g.ws + ws_index(p, BM, BN, lt, chunk, ly * TM + i, lx * TN);
                     uint32_t w[(TN + 1) / 2];
 #pragma unroll
                     for (int j = 0; j < TN; j += 2) {
@@ -469,11 +469,10 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                         w[j / 2] = c;
                     }
                     if (TN == 1) {
-                        dst[i * BN] = (uint16_t)w[0];
+                        dst[0] = (uint16_t)w[0];
                     } else {
 #pragma unroll
-                        for (int j = 0; j < TN / 2; ++j)
-                            reinterpret_cast<uint32_t*>(dst + i * BN)[j] = w[j];
+                        for (int j = 0; j < TN / 2; ++j) reinterpret_cast<uint32_t*>(dst)[j] = w[j];
                     }
                 }
             } else {
