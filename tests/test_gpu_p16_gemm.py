@@ -2,7 +2,7 @@
 chunk-based FP16 accumulation) with the oracle, bit for bit: every layout,
 ragged chunks, CL = 1 and CL >= K, whole and shared-out tiles, subnormal and
 overflowing products, specials, K = 0, and the last layer of the speech DNN
-(256 x 6000 x 1024 and its backward GEMMs) on sampled outputs."""
+(256 x 6000 x 1024 and its backward GEMMs) on one output per 16 x 16 block."""
 import numpy as np
 import pytest
 import torch
@@ -121,9 +121,14 @@ def test_p16_gemm_empty_k():
     assert np.all(host(C) == 0)
 
 
-def test_p16_gemm_last_layer_shapes():
+def test_p16_gemm_last_layer_shapes(monkeypatch):
     """The speech DNN's last layer (1024 -> 6000, batch 256): Forward,
-    Backward (trans_b) and Gradient (trans_a) GEMMs, sampled outputs."""
+    Backward (trans_b) and Gradient (trans_a) GEMMs in the plan the benchmark
+    runs (workspace from the query), one output in every 16 x 16 block of C
+    -- the smallest workgroup tile, so every tile and every shared tile's
+    pieces are checked -- plus the corners; for the two GEMMs with tiles
+    shared out, also with the guard off (the 2^96 path throughout)."""
+    from tests.test_gpu_workloads import tile_points
     rng = np.random.default_rng(986)
     X = p16(np.maximum(rng.standard_normal((256, 1024)), 0))
     W = p16(rng.standard_normal((1024, 6000)) / 32.0)
@@ -133,9 +138,14 @@ def test_p16_gemm_last_layer_shapes():
             (X, W, Xd, Wd, 256, 6000, 1024, 0, 0, "fwd"),
             (E, W, Ed, Wd, 256, 1024, 6000, 0, 1, "dgrad"),
             (X, E, Xd, Ed, 1024, 6000, 256, 1, 0, "wgrad")):
-        say(f"chunk_gemm_p16 last layer {what} {M}x{N}x{K}")
-        got = gemm16(Ad, Bd, M, N, K, 64, ta, tb)
-        r = np.concatenate([rng.integers(0, M, 300), [0, M - 1, M - 1]])
-        c = np.concatenate([rng.integers(0, N, 300), [N - 1, 0, N - 1]])
+        r, c = tile_points(M, N, 990 + ta + 2 * tb, block=16, per=1)
+        say(f"chunk_gemm_p16 last layer {what} {M}x{N}x{K}: {r.size} outputs checked")
         ref = oracle.chunk_gemm_p16_points(A, B, 64, r, c, ta, tb)
-        assert np.array_equal(got[r, c], ref), what
+        got = gemm16(Ad, Bd, M, N, K, 64, ta, tb)
+        assert np.array_equal(got[r, c], ref), (what, np.flatnonzero(got[r, c] != ref)[:5])
+        if fp8t.chunk_gemm_p16_workspace_size(ta, tb, M, N, K, 64) > 0:
+            monkeypatch.setenv("FP8T_GEMM_GUARD", "0")
+            say(f"chunk_gemm_p16 last layer {what}, guard off")
+            got = gemm16(Ad, Bd, M, N, K, 64, ta, tb)
+            monkeypatch.delenv("FP8T_GEMM_GUARD")
+            assert np.array_equal(got[r, c], ref), (what, np.flatnonzero(got[r, c] != ref)[:5])
