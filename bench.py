@@ -50,7 +50,7 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 300.0 MB, weight-gradient 2402.6 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "79061d69458555e3464201610375fbab4292ca5ebef98c1c31d9ba613dbac90a"
+TRAFFIC_SOURCES_SHA256 = "66cd3ab8719a49d863049a3939729b4f58eac1c0f268f5899285212d38abb5b5"
 EXACT_TRAFFIC_BYTES_PER_CALL = 964.2e6
 
 
