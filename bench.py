@@ -521,7 +521,7 @@ def conv_measurement(torch, fp8t, W8, D8, u8, u16):
         out = u16(rows, Cout)
         f = fp8t.conv2d_wgrad_fp8 if wg else fp8t.conv2d_fwd_fp8
         t = time_ms(torch, lambda: f(X8, N, H, W, C, 3, 3, 1, 1, B, Cout, CL, out, Cout, ws, wb),
-                    3)
+                    10)
         res[name] = {"ms": t, "tmac_s": M * K * Cout / (t * 1e-3) / 1e12,
                      "frac_of_valu_emulation_peak": M * K * Cout / (t * 1e-3) /
                      exact_peak_mac_s(CL)}
