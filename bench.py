@@ -118,6 +118,9 @@ def parse():
                    help="skip the measurements outside the timed step (profiling runs)")
     p.add_argument("--cpu-seconds", type=float, default=20.0,
                    help="target wall time of the oracle sample")
+    p.add_argument("--only", choices=sorted(ONLY),
+                   help="run one of the measurements outside the timed step by itself and "
+                        "print its JSON (profiling runs); no timed step")
     return p.parse_args()
 
 
@@ -358,7 +361,7 @@ def sweep_measurement(torch, fp8t):
                 wb = fp8t.chunk_gemm_workspace_size(1, 0, 512, 512, K, cl, mode)
                 ws = torch.empty(wb, dtype=torch.uint8, device="cuda") if wb else None
                 ms = time_ms(torch, lambda: fp8t.chunk_gemm(1, 0, 512, 512, K, cl, A8, 512, B8,
-                                                            512, C, 512, mode, ws, wb), 3)
+                                                            512, C, 512, mode, ws, wb), 5)
                 peak, kind = mode_peak(mode == 1, min(cl, K), K)
                 rate = 512 * 512 * K / (ms * 1e-3)
                 got = p16[C.view(torch.int16).long() & 0xFFFF]
@@ -563,6 +566,13 @@ def mlp_measurement(torch, fp8t):
     return res
 
 
+# the measurements outside the timed step that --only runs by themselves
+ONLY = {"sweep": lambda torch, fp8t: sweep_measurement(torch, fp8t),
+        "small": lambda torch, fp8t: small_measurement(torch, fp8t),
+        "speech_layers": lambda torch, fp8t: speech_layers_measurement(torch, fp8t),
+        "p16_last_layer": lambda torch, fp8t: p16_last_layer_measurement(torch, fp8t)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -572,6 +582,13 @@ def main():
     import torch
     import paper_1812_08011_amd as fp8t
     import workloads
+
+    if args.only:
+        torch.cuda.set_device(0)
+        fp8t.lib()
+        print(json.dumps({"only": args.only, "kernels": {args.only: ONLY[args.only](torch, fp8t)}}),
+              flush=True)
+        return
 
     dev = "cuda:0"
     torch.cuda.set_device(0)

@@ -203,6 +203,14 @@ double valu_ops_per_mac(int cfg) {
 // gfx950 about four waves per SIMD are needed to issue every cycle whatever
 // the outputs per lane (measured: a 2 x 2 register tile at one wave per SIMD
 // runs at a quarter of the rate a 1 x 1 tile reaches at four).
+// VALU instructions per multiply-accumulate the fast chain kernel saves over
+// the exact one (measured on 512 x 512 outputs, K 16384 and 65536, CL 8 and
+// 12): the rounding after each FMA goes, worth more on the 2 x 2 tile than
+// on the narrower ones.
+double chain_fast_saving(int cfg) {
+    return cfg == kChainConfig ? 3.0 : cfg == kChainConfig + 1 ? 2.3 : 2.6;
+}
+
 double valu_efficiency(double w) { return w >= 4.0 ? 1.0 : w / 4.0; }
 
 // Extra VALU instructions per multiply-accumulate with FP16 operands: the
@@ -277,16 +285,18 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 t_out = mfma_cost_per_output_chunk(cfg, CL);
                 t_tile = mfma_cost_per_tile(cfg);
             } else {
-                // the chain kernel: exact mode, 4-k groups inside one chunk
-                if (is_chain(cfg) && (fast || conv || p16 || (CL % 4 != 0 && CL < K))) continue;
+                // the chain kernel: 4-k groups inside one chunk
+                if (is_chain(cfg) && (conv || p16 || (CL % 4 != 0 && CL < K))) continue;
                 const ValuShape sh = valu_shape(cfg);
                 fn = conv ? valu_conv_kernel(cfg, ta)
                    : p16  ? valu_p16_kernel(cfg, ta, tb)
                           : valu_kernel(cfg, ta, tb, fast);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
                 // the MACs of a chunk, and its end (an add and a rounding); an
-                // FP16 product costs its multiplication and rounding on top
-                const double ops = valu_ops_per_mac(cfg) + (p16 ? kP16ProductOps : 0.0);
+                // FP16 product costs its multiplication and rounding on top,
+                // and the fast chain kernel does without the rounding
+                const double ops = valu_ops_per_mac(cfg) + (p16 ? kP16ProductOps : 0.0) -
+                                   (fast && is_chain(cfg) ? chain_fast_saving(cfg) : 0.0);
                 t_out = ((double)CL * ops + 4.0) / (kLanesPerCU * kClockHz);
             }
             if (!fn) continue;

@@ -1,6 +1,7 @@
-// chunk_gemm, exact mode, for GEMMs with few outputs and long dot products
-// (the long-accumulation Gradient GEMMs of Sec. 4.2 / Fig. 6, and the
-// sequential FP16 sums of Fig. 3(b)).
+// chunk_gemm for GEMMs with few outputs and long dot products (the
+// long-accumulation Gradient GEMMs of Sec. 4.2 / Fig. 6, and the sequential
+// FP16 sums of Fig. 3(b)): the exact mode, and the fast mode for chunk
+// lengths the matrix cores cannot split.
 //
 // Every output's chain of rounded FP16 additions (Sec. 2.3, Fig. 3(a)) is
 // sequential in k; K can be shared out over workgroups only at chunk
@@ -20,7 +21,10 @@
 // 64 are double-buffered from HBM.  Per multiply-accumulate it issues the FMA
 // and the rounding of the exact-mode kernels (guarded: plain values,
 // Veltkamp; safe: scaled by 2^96, integer rounding, for tiles that fail the
-// overflow guard), with the same bits.
+// overflow guard), with the same bits.  FAST: a chunk is summed in plain FP32
+// (one FMA per multiply-accumulate) and rounded to FP16 once at its end, then
+// added into the running sum in the 2^96 domain -- the arithmetic of the
+// fast-mode variant of the main VALU kernel, with no guard needed.
 //
 // Chunk lengths must be multiples of 4 (the 4-k groups never straddle a
 // chunk boundary) or cover K; CL = 1 reaches this kernel as CL = K (the same
@@ -71,7 +75,7 @@ __device__ __forceinline__ void store_rowk(float* lds, int tid, const uint32_t (
     }
 }
 
-template <int TM, int TN, bool TA, bool TB>
+template <int TM, int TN, bool TA, bool TB, bool FAST>
 __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
     constexpr int BM = 16 * TM, BN = 16 * TN;
     constexpr int WA = BM * kBK / 4 / kNT, WB = BN * kBK / 4 / kNT;   // words per thread
@@ -97,6 +101,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
     auto tile_pass = [&](auto safe_tag, int64_t tile) __attribute__((always_inline)) -> bool {
         constexpr bool SAFE = decltype(safe_tag)::value;
         constexpr int DOM = SAFE ? 96 : 0;
+        constexpr int ASHIFT = FAST ? 0 : DOM;   // the fast mode sums plain products
         constexpr bool TRACK = !SAFE;
         int tr, tc;
         tile_rc(p, tile, tr, tc);
@@ -133,6 +138,8 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
                     for (int j = 0; j < TN; ++j) {
                         if (q == 0 && fresh)
                             P[i][j] = __builtin_fmaf(av[i][q], bv[j][q], 0.0f);
+                        else if (FAST)
+                            P[i][j] = __builtin_fmaf(av[i][q], bv[j][q], P[i][j]);
                         else
                             P[i][j] = rnd(__builtin_fmaf(av[i][q], bv[j][q], P[i][j]));
                     }
@@ -142,7 +149,9 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
             for (int i = 0; i < TM; ++i)
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
-                    S[i][j] = rnd(S[i][j] + P[i][j]);
+                    // fast: the FP32 chunk sum rounded to FP16 in the 2^96 domain
+                    const float pv = FAST ? rn16s(P[i][j] * 0x1p96f) : P[i][j];
+                    S[i][j] = rnd(S[i][j] + pv);
                     if (TRACK) smax = max3_abs(smax, S[i][j], S[i][j]);
                 }
         };
@@ -160,7 +169,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
         int crem = clg;                  // groups left in the current chunk
         valu_impl::slab_load<KCA, BM, kBK, kNT, WA>(g.A, g.lda, g.a_vec, m0, g.M, 0, g.K, tid, ra);
         valu_impl::slab_load<KCB, BN, kBK, kNT, WB>(g.B, g.ldb, g.b_vec, n0, g.N, 0, g.K, tid, rb);
-        store_rowk<KCA, BM, WA, DOM, TRACK>(As[0], tid, ra, amax_a, special);
+        store_rowk<KCA, BM, WA, ASHIFT, TRACK>(As[0], tid, ra, amax_a, special);
         store_rowk<KCB, BN, WB, 0, TRACK>(Bs[0], tid, rb, amax_b, special);
         __syncthreads();
         for (int s = 0; s < nslabs; ++s) {
@@ -196,7 +205,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
                 }
             }
             if (s + 1 < nslabs) {
-                store_rowk<KCA, BM, WA, DOM, TRACK>(As[buf ^ 1], tid, ra, amax_a, special);
+                store_rowk<KCA, BM, WA, ASHIFT, TRACK>(As[buf ^ 1], tid, ra, amax_a, special);
                 store_rowk<KCB, BN, WB, 0, TRACK>(Bs[buf ^ 1], tid, rb, amax_b, special);
             }
             __syncthreads();
@@ -259,27 +268,33 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
     for (int64_t t = blockIdx.x; t < p.t_whole; t += p.G) {
         const int64_t tile = whole_tile(p, t);
         bool done = false;
-        if (g.guarded) done = tile_pass(std::integral_constant<bool, false>{}, tile);
+        // the fast mode has the 2^96-domain path only
+        if (!FAST && g.guarded) done = tile_pass(std::integral_constant<bool, false>{}, tile);
         if (!done) tile_pass(std::integral_constant<bool, true>{}, tile);
     }
 }
 
-template <int TM, int TN>
+template <int TM, int TN, bool FAST>
 const void* chain_sel(int ta, int tb) {
-    if (ta) return tb ? reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, true, true>)
-                      : reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, true, false>);
-    return tb ? reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, false, true>)
-              : reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, false, false>);
+    if (ta) return tb ? reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, true, true, FAST>)
+                      : reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, true, false, FAST>);
+    return tb ? reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, false, true, FAST>)
+              : reinterpret_cast<const void*>(&chunk_gemm_chain<TM, TN, false, false, FAST>);
+}
+
+template <bool FAST>
+const void* chain_shape(int shape, int ta, int tb) {
+    switch (shape) {
+        case 0: return chain_sel<2, 2, FAST>(ta, tb);
+        case 1: return chain_sel<1, 2, FAST>(ta, tb);
+        default: return chain_sel<1, 1, FAST>(ta, tb);
+    }
 }
 
 }  // namespace
 
-const void* chain_kernel(int shape, int ta, int tb) {
-    switch (shape) {
-        case 0: return chain_sel<2, 2>(ta, tb);
-        case 1: return chain_sel<1, 2>(ta, tb);
-        default: return chain_sel<1, 1>(ta, tb);
-    }
+const void* chain_kernel(int shape, int ta, int tb, int fast) {
+    return fast ? chain_shape<true>(shape, ta, tb) : chain_shape<false>(shape, ta, tb);
 }
 
 }  // namespace fp8t

@@ -14,8 +14,8 @@ struct ValuShape {
 
 // Configurations 0-8 are chunk_gemm_valu register tiles (gemm_valu_impl.h);
 // configurations 9, 10, 11 are chunk_gemm_chain (gemm_chain.hip) with 2 x 2,
-// 1 x 2 and 1 x 1 outputs per lane: exact mode only, whole tiles, CL a
-// multiple of 4 or covering K.
+// 1 x 2 and 1 x 1 outputs per lane: whole tiles, CL a multiple of 4 or
+// covering K.
 constexpr int kValuConfigs = 12;
 constexpr int kChainConfig = 9;
 inline bool is_chain(int cfg) { return cfg >= kChainConfig && cfg < kChainConfig + 3; }
@@ -39,7 +39,8 @@ const void* valu_p16_kernel(int cfg, int ta, int tb);
 const void* valu_conv_kernel(int cfg, int ta);
 
 // chunk_gemm_chain with 2 x 2 (shape 0), 1 x 2 (1) or 1 x 1 (2) outputs per
-// lane for the given operand layouts (gemm_chain.hip).
-const void* chain_kernel(int shape, int ta, int tb);
+// lane for the given operand layouts and mode (fast: sum a chunk in FP32 and
+// round once) (gemm_chain.hip).
+const void* chain_kernel(int shape, int ta, int tb, int fast);
 
 }  // namespace fp8t

@@ -29,7 +29,7 @@ ValuShape valu_shape(int cfg) {
 
 const void* valu_kernel(int cfg, int ta, int tb, int fast) {
     if (cfg < 0 || cfg >= kValuConfigs) return nullptr;
-    if (is_chain(cfg)) return fast ? nullptr : chain_kernel(cfg - kChainConfig, ta, tb);
+    if (is_chain(cfg)) return chain_kernel(cfg - kChainConfig, ta, tb, fast);
     if (!ta && !tb) return valu_kernel_nn(cfg, fast);
     if (!ta && tb) return valu_kernel_nt(cfg, fast);
     if (ta && !tb) return valu_kernel_tn(cfg, fast);

@@ -292,6 +292,37 @@ def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
             assert np.array_equal(Cg, oracle.chunk_gemm(A, B, CL, ta, tb))
 
 
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_chunk_gemm_fast_vector_alu_tiles_same_bits(ta, tb, monkeypatch):
+    """The fast mode for chunk lengths the matrix cores cannot split (CL not
+    a multiple of 16): every vector-ALU kernel that has it -- the register
+    tiles 4, 5, 6 of the main kernel and the chain kernel's 2 x 2, 1 x 2 and
+    1 x 1 (9, 10, 11) -- sums a chunk's products in FP32 in ascending k and
+    rounds once, so all give the same bits: ragged M, N and K (a last 4-k
+    group with zero-filled products), CL 4 to 36, Inf/NaN operands; within
+    the fast oracle's bounds."""
+    rng = np.random.default_rng(700 + 2 * ta + tb)
+    shapes = [(130, 67, 333, 8), (64, 96, 1000, 12), (33, 47, 700, 4), (70, 150, 602, 20),
+              (5, 3, 17, 4), (128, 64, 2048, 36)]
+    for si, (M, N, K, CL) in enumerate(shapes):
+        A, B = _operands(rng, M, N, K, ta, tb)
+        if si == 1:
+            (A.T if ta else A)[5, 900] = 0x7C          # +Inf
+            (A.T if ta else A)[60, 500] = 0x7F         # NaN
+        Ad, Bd = dev(A), dev(B)
+        got = {}
+        for tile in ("6", "4", "5", "9", "10", "11"):
+            monkeypatch.setenv("FP8T_VALU_TILE", tile)
+            say(f"fast vector-ALU tile={tile} ta={ta} tb={tb} {M}x{N}x{K} CL={CL}")
+            got[tile] = host(gemm(Ad, Bd, M, N, K, CL, ta, tb, mode=fp8t.FAST))
+        monkeypatch.delenv("FP8T_VALU_TILE")
+        for tile, C in got.items():
+            assert np.array_equal(C, got["6"]), (tile, M, N, K, CL,
+                                                 np.argwhere(C != got["6"])[:5])
+        Co = oracle.chunk_gemm(A, B, CL, ta, tb, mode=oracle.FAST)
+        check_fast(got["6"], A, B, CL, ta, tb, f"fast valu {M}x{N}x{K} CL={CL}", Co=Co)
+
+
 @pytest.mark.parametrize("mtile", ["0", "1", "2"])
 @pytest.mark.parametrize("wgs", ["2", "9"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (1, 0), (0, 1)])
