@@ -34,15 +34,28 @@ namespace {
 // ---------------------------------------------------------------------------
 
 // FP16 code -> value * 2^96 without branches (the fold pass decodes one code
-// per output per chunk): normal, Inf and NaN codes map by placing the code's
-// exponent and significand in the FP32 fields; zero and subnormals (m 2^-39)
-// convert the significand.
-__device__ __forceinline__ float fp16_to_f32s_fold(uint32_t c) {
-    const uint32_t mag = c & 0x7FFFu;
-    const float fn = __uint_as_float((mag << 14) + (192u << 23));
-    const float fs = (float)(c & 0x1FFu) * 0x1p57f;
-    const float f = mag >= 0x200u ? fn : fs;
-    return __uint_as_float(__float_as_uint(f) | ((c & 0x8000u) << 16));
+// per output per chunk).  Normal, Inf and NaN codes by placing the code's
+// fields in FP32's: the code sign-extended to 32 bits and shifted left by 14
+// has the sign in bits 29-31, the exponent in 23-28 and the significand in
+// 14-22, so setting bits 29 and 30 adds the scaled domain's 192 to the
+// exponent (63, Inf and NaN, lands on 255).  Zero and subnormal codes
+// (exponent 0) come out as +-(2^65 + m 2^56), whose value is +-m 2^57: the
+// magnitude 2 |x| - 2^66, one exact FMA.  For every other code that FMA gives
+// a magnitude >= |x|, so the result is the operand of smaller magnitude: with
+// x's sign put on the FMA's (non-negative) result, the smaller of the two bit
+// patterns as unsigned integers (both NaN for a NaN code; -0 stays -0).
+__device__ __forceinline__ float fold_decode(int32_t code_sx) {
+    const uint32_t u = ((uint32_t)code_sx << 14) | 0x60000000u;
+    const float y = fmaf(fabsf(__uint_as_float(u)), 2.0f, -0x1p66f);
+    const uint32_t ys = __float_as_uint(y) | (u & 0x80000000u);
+    return __uint_as_float(min(u, ys));
+}
+// the code in bits 0-15 / 16-31 of w
+__device__ __forceinline__ float fold_decode_lo(uint32_t w) {
+    return fold_decode(__builtin_amdgcn_sbfe((int32_t)w, 0, 16));
+}
+__device__ __forceinline__ float fold_decode_hi(uint32_t w) {
+    return fold_decode(__builtin_amdgcn_sbfe((int32_t)w, 16, 16));
 }
 
 // Each thread takes kFoldV consecutive outputs of one row of a shared tile and
@@ -97,24 +110,32 @@ __global__ __launch_bounds__(kFoldT) void chunk_fold(GemmArgs g, Plan p, int BM,
     const int nv = min(kFoldV, g.N - n0);
     float S[kFoldV];
 #pragma unroll
-    for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fp16_to_f32s_fold(sp[v]) : 0.0f;
+    for (int v = 0; v < kFoldV; ++v) S[v] = v < nv ? fold_decode_lo(sp[v]) : 0.0f;
     const FoldVec* src = reinterpret_cast<const FoldVec*>(g.ws + ws_index(p, BM, BN, lt, 0, r, c));
-    const int64_t step = 4 * BN / kFoldV;       // vectors per chunk of a band
+    const int step = 4 * BN / kFoldV;           // vectors per chunk of a band
     auto add = [&](FoldVec q) __attribute__((always_inline)) {
         uint32_t w[kFoldV / 2];
         __builtin_memcpy(w, &q, sizeof(q));
 #pragma unroll
         for (int v = 0; v < kFoldV; ++v)
-            S[v] = rn16s(S[v] + fp16_to_f32s_fold((w[v / 2] >> (16 * (v % 2))) & 0xFFFFu));
+            S[v] = rn16s(S[v] + (v % 2 ? fold_decode_hi(w[v / 2]) : fold_decode_lo(w[v / 2])));
     };
     // two batches of kFoldU chunks: one in flight while the other is added.
     // Every batch load is unconditional (chunk indices clamped to the last
     // chunk, the extra values never added), so the compiler waits for the
     // older batch only; a conditional load makes it wait for both.
+    // A batch that lies inside the tile's chunks loads from one base pointer
+    // at uniform offsets; only the last one clamps each index.
     const int last = p.nch - 1;
     auto load = [&](FoldVec (&q)[kFoldU], int c0) __attribute__((always_inline)) {
+        if (c0 + kFoldU <= p.nch) {
+            const FoldVec* b = src + (int64_t)c0 * step;
 #pragma unroll
-        for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)min(c0 + u, last) * step];
+            for (int u = 0; u < kFoldU; ++u) q[u] = b[u * step];
+        } else {
+#pragma unroll
+            for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)min(c0 + u, last) * step];
+        }
     };
     auto fold_all = [&](const FoldVec (&q)[kFoldU]) __attribute__((always_inline)) {
 #pragma unroll
