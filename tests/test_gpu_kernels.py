@@ -241,6 +241,50 @@ def test_chunk_gemm_exact_shared_tiles(tile, wgs, ta, tb, monkeypatch):
         assert np.array_equal(Cg, Co), (M, N, K, CL, np.argwhere(Cg != Co)[:5])
 
 
+@pytest.mark.parametrize("guard", ["1", "0"])
+@pytest.mark.parametrize("wgs", ["3", "7"])
+def test_chunk_gemm_fold_decodes_every_kind_of_chunk_sum(wgs, guard, monkeypatch):
+    """Shared tiles only, so the fold pass continues every output over chunk
+    sums of each kind: zeros (rows of -0 / +0 codes), FP16 subnormals of both
+    signs (one 2^-16 x 2^-16 product per chunk: 2^-32), normal values, an Inf
+    chunk and a NaN chunk part-way along K.  The fold decodes each chunk
+    sum's FP16 code and must give the oracle's bits."""
+    monkeypatch.setenv("FP8T_GEMM_SPLIT", "1")
+    monkeypatch.setenv("FP8T_GEMM_WGS", wgs)
+    monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+    rng = np.random.default_rng(591)
+    M, N, CL, nch = 10, 64, 64, 40
+    K = CL * nch
+    A = np.zeros((M, K), np.uint8)
+    A[0, :] = 0x80                                   # -0
+    A[1, :] = 0x00                                   # +0
+    A[2, ::CL] = 0x01                                # 2^-16, one per chunk
+    A[3, ::CL] = 0x81                                # -2^-16
+    A[4, ::CL] = np.where(rng.random(nch) < 0.5, 0x01, 0x81)
+    A[4, 5::CL] = np.where(rng.random(nch) < 0.5, 0x02, 0x82)
+    A[5, :] = rng.integers(0x30, 0x48, K) | (rng.integers(0, 2, K) << 7)
+    A[6, :] = A[5, :]
+    A[6, CL * 20 + 3] = 0x7C                         # +Inf in chunk 20
+    A[7, :] = A[5, :]
+    A[7, CL * 11 + 9] = 0x7D                         # NaN in chunk 11
+    A[8, :] = 0x80
+    A[8, CL * 30] = 0x01                             # -0 until chunk 30
+    A[9, ::CL] = 0x81
+    A[9, CL * 35:] = 0x00                            # negative subnormal sums, then +0
+    B = np.empty((K, N), np.uint8)
+    B[:, :32] = 0x01                                 # 2^-16: subnormal products
+    B[:, 32:] = rng.integers(0x30, 0x48, (K, 32)) | (rng.integers(0, 2, (K, 32)) << 7)
+    B[:, 40] = 0x3C                                  # 1.0
+    ws = fp8t.chunk_gemm_workspace_size(0, 0, M, N, K, CL, fp8t.EXACT)
+    assert ws > 0
+    say(f"fold decodes every kind of chunk sum wgs={wgs} guard={guard}")
+    Cg = host(gemm(dev(A), dev(B), M, N, K, CL))
+    Co = oracle.chunk_gemm(A, B, CL)
+    assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
+    assert np.all(Cg[:2] == 0)
+    assert np.all((Cg[6] & 0x7FFF) == 0x7E00) and np.all(Cg[7] == 0x7F00)
+
+
 def test_chunk_gemm_workspace_contract():
     """No workspace: a plan that needs none, same bits.  Too small a
     workspace is rejected before anything is enqueued."""
