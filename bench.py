@@ -182,10 +182,17 @@ def host_cpu_model():
     return "unknown"
 
 
-def time_ms(torch, fn, reps):
+def time_ms(torch, fn, reps, warm_s=0.03):
     """Average milliseconds of fn() over reps calls, from HIP events on the
-    current stream (the one the library launches on), after one warm-up."""
+    current stream (the one the library launches on), after warm-up calls
+    for at least warm_s seconds (the first calls after host-side work or an
+    idle gap run at lower clocks)."""
     fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < warm_s:
+        fn()
+        torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(reps):
