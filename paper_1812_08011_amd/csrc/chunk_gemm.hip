@@ -563,6 +563,7 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     g.a_vec16 = !p16 && aligned(A, 16) && lda % 16 == 0;
     g.b_vec16 = !p16 && aligned(B, 16) && ldb % 16 == 0;
     g.c_vec = C && aligned(C, 4) && ldc % 2 == 0;
+    g.c_vec8 = C && aligned(C, 8) && ldc % 4 == 0;
     g.c_vec16 = C && aligned(C, 16) && ldc % 8 == 0;
     g.c8_vec8 = C8 && aligned(C8, 8) && ldc8 % 8 == 0;
     g.c8_vec4 = C8 && aligned(C8, 4) && ldc8 % 4 == 0;
@@ -699,6 +700,7 @@ int conv_gemm_call(bool wgrad, const uint8_t* X, int64_t N, int64_t H, int64_t W
     g.a_vec = 0;
     g.b_vec = aligned(B, 4) && Cout % 4 == 0 && Cout < (1 << 24);
     g.c_vec = aligned(Out, 4) && ldo % 2 == 0;
+    g.c_vec8 = aligned(Out, 8) && ldo % 4 == 0;
     g.c_vec16 = aligned(Out, 16) && ldo % 8 == 0;
     g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
     g.conv.H = (int)H;

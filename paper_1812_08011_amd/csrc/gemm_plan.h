@@ -54,6 +54,7 @@ struct GemmArgs {
     int a_vec16;        // A, lda allow 16-byte loads
     int b_vec16;        // B, ldb allow 16-byte loads
     int c_vec;          // C, ldc allow 4-byte stores of code pairs
+    int c_vec8;         // C, ldc allow 8-byte stores (4 codes)
     int c_vec16;        // C, ldc allow 16-byte stores (8 codes)
     int c8_vec8;        // C8, ldc8 allow 8-byte stores
     int c8_vec4;        // C8, ldc8 allow 4-byte stores

@@ -224,6 +224,22 @@ __device__ __forceinline__ uint32_t row_min(uint32_t m) {
     return min(m, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)m, 0x121 /* row_ror:1 */, 0xF, 0xF, false));
 }
 
+// op (max or or) over all 64 lanes of a wave, in every lane: DPP rotations
+// within 16-lane rows, then the 16- and 32-lane swaps (a chain of cheap
+// VALU steps; a shuffle through the LDS crossbar per step cost the tile end
+// a long dependent latency).
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce(uint32_t x, Op op) {
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x128 /* row_ror:8 */, 0xF, 0xF, false));
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x124 /* row_ror:4 */, 0xF, 0xF, false));
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x122 /* row_ror:2 */, 0xF, 0xF, false));
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x121 /* row_ror:1 */, 0xF, 0xF, false));
+    const auto t16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    x = op(x, op((uint32_t)t16[0], (uint32_t)t16[1]));
+    const auto t32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return op(x, op((uint32_t)t32[0], (uint32_t)t32[1]));
+}
+
 template <int G>
 __device__ __forceinline__ uint32_t lanes_mod_min(uint32_t m) {
     static_assert(G == 8 || G == 16, "lanes equal modulo 8 or 16");
@@ -635,13 +651,13 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             uint32_t* st = s_track[gslot];
             uint32_t ua = __float_as_uint(amax_a), ub = __float_as_uint(amax_b), us = special;
             uint32_t uS = __float_as_uint(smax);
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) {      // non-negative floats: bit order
-                ua = max(ua, (uint32_t)__shfl_xor((int)ua, o));
-                ub = max(ub, (uint32_t)__shfl_xor((int)ub, o));
-                us |= (uint32_t)__shfl_xor((int)us, o);
-                uS = max(uS, (uint32_t)__shfl_xor((int)uS, o));
-            }
+            // non-negative floats: bit order
+            auto umax = [](uint32_t x, uint32_t y) __attribute__((always_inline)) { return max(x, y); };
+            auto uor = [](uint32_t x, uint32_t y) __attribute__((always_inline)) { return x | y; };
+            ua = wave_reduce(ua, umax);
+            ub = wave_reduce(ub, umax);
+            us = wave_reduce(us, uor);
+            uS = wave_reduce(uS, umax);
             if ((tid & 63) == 0) {
                 atomicMax(&st[0], ua);
                 atomicMax(&st[1], ub);
@@ -678,10 +694,12 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             return true;
         }
         // The running sum: a lane's TN consecutive codes of a row are stored
-        // in pairs when the whole row lies inside C and is aligned; the FP8
-        // result (whole tiles only: shared tiles get it from the fold pass)
-        // four codes per 4-byte store under the same conditions, else byte
-        // by byte.
+        // four per 8-byte store (the 16 lanes of a row then write whole
+        // 128-byte lines; 4-byte stores half-filled lines and cost the
+        // Backward-data GEMM, which writes 231 MB, 3%), else in pairs, when
+        // the whole row lies inside C and is aligned; the FP8 result (whole
+        // tiles only: shared tiles get it from the fold pass) four codes per
+        // 4-byte store under the same conditions, else byte by byte.
         const int nl = n0 + lx * TN;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
@@ -689,7 +707,17 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
             if (m >= g.M) continue;
             if (g.C) {
                 uint16_t* crow = g.C + (int64_t)m * g.ldc + nl;
-                if (TN > 1 && g.c_vec && nl + TN <= g.N) {
+                if (TN % 4 == 0 && g.c_vec8 && nl + TN <= g.N) {
+#pragma unroll
+                    for (int j = 0; j < TN; j += 4) {
+                        uint2 c;
+                        c.x = (uint32_t)f32d_to_fp16<DOM>(S[i][j]) |
+                              ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 1]) << 16);
+                        c.y = (uint32_t)f32d_to_fp16<DOM>(S[i][j + 2]) |
+                              ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 3]) << 16);
+                        reinterpret_cast<uint2*>(crow)[j / 4] = c;
+                    }
+                } else if (TN > 1 && g.c_vec && nl + TN <= g.N) {
 #pragma unroll
                     for (int j = 0; j < TN; j += 2) {
                         uint32_t c = (uint32_t)f32d_to_fp16<DOM>(S[i][j]) |
