@@ -50,8 +50,8 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 300.0 MB, weight-gradient 2402.6 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "28ec6f9ebd4a162174511da6663f4442bc2aba4038a945f4a089bfe04b2ce4f6"
-EXACT_TRAFFIC_BYTES_PER_CALL = 964.1e6
+TRAFFIC_SOURCES_SHA256 = "031a3056eff15241e7b017ad641ac1e5ff04406cdc309b7f4a27a02b7bea6b06"
+EXACT_TRAFFIC_BYTES_PER_CALL = 964.4e6
 
 
 # The sources that decide what an exact-mode chunk_gemm call runs: the VALU
