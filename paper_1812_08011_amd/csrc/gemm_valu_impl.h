@@ -211,10 +211,6 @@ __device__ __forceinline__ void slab_load16(const uint16_t* __restrict__ ptr, in
     }
 }
 
-// Minimum of m over the lanes of a wave equal modulo G (G 8 or 16: lane
-// bits log2 G .. 5), in every lane: a DPP rotation by 8 within 16-lane rows,
-// then gfx950's 16- and 32-lane swaps (each returns both registers' swapped
-// halves; their minimum with m is the partner lane's value or m's own).
 // Minimum of m over each 16-lane row, in every lane (DPP rotations by 8, 4,
 // 2 and 1 within the row).
 __device__ __forceinline__ uint32_t row_min(uint32_t m) {
@@ -225,9 +221,9 @@ __device__ __forceinline__ uint32_t row_min(uint32_t m) {
 }
 
 // op (max or or) over all 64 lanes of a wave, in every lane: DPP rotations
-// within 16-lane rows, then the 16- and 32-lane swaps (a chain of cheap
-// VALU steps; a shuffle through the LDS crossbar per step cost the tile end
-// a long dependent latency).
+// within 16-lane rows, then the 16- and 32-lane swaps -- VALU steps instead
+// of shuffles through the LDS crossbar (measured: Backward-data and Gradient
+// GEMMs of the conv stage 1.5-2% faster, Forward 1% slower).
 template <typename Op>
 __device__ __forceinline__ uint32_t wave_reduce(uint32_t x, Op op) {
     x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x128 /* row_ror:8 */, 0xF, 0xF, false));
@@ -240,6 +236,10 @@ __device__ __forceinline__ uint32_t wave_reduce(uint32_t x, Op op) {
     return op(x, op((uint32_t)t32[0], (uint32_t)t32[1]));
 }
 
+// Minimum of m over the lanes of a wave equal modulo G (G 8 or 16: lane
+// bits log2 G .. 5), in every lane: a DPP rotation by 8 within 16-lane rows,
+// then gfx950's 16- and 32-lane swaps (each returns both registers' swapped
+// halves; their minimum with m is the partner lane's value or m's own).
 template <int G>
 __device__ __forceinline__ uint32_t lanes_mod_min(uint32_t m) {
     static_assert(G == 8 || G == 16, "lanes equal modulo 8 or 16");
@@ -262,7 +262,7 @@ __device__ __forceinline__ uint32_t lanes_mod_min(uint32_t m) {
 // rows: 16-lane runs), they first take their minima across lanes and one of
 // them updates kmin, instead of every lane's atomic on the same LDS address
 // (FP16-operand GEMMs of the 1024 -> 6000 layer, Forward / Backward /
-// Gradient: 0.292 / 0.333 / 0.220 -> 0.285 / 0.285 / 0.225 ms).  Elsewhere
+// Gradient: 0.292 / 0.333 / 0.220 -> 0.283 / 0.285 / 0.221 ms).  Elsewhere
 // the reduction measured slower than the atomics (32-lane runs; tiles of 32
 // rows, with 8 times less compute per staged word).
 template <bool KC, int R, int BK, int NT, int W, int SH, bool TRACK>
@@ -695,8 +695,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
         }
         // The running sum: a lane's TN consecutive codes of a row are stored
         // four per 8-byte store (the 16 lanes of a row then write whole
-        // 128-byte lines; 4-byte stores half-filled lines and cost the
-        // Backward-data GEMM, which writes 231 MB, 3%), else in pairs, when
+        // 128-byte lines with one instruction), else in pairs, when
         // the whole row lies inside C and is aligned; the FP8 result (whole
         // tiles only: shared tiles get it from the fold pass) four codes per
         // 4-byte store under the same conditions, else byte by byte.
