@@ -11,8 +11,10 @@
 //   MFMA instruction's K (16);
 // * chunk_gemm_mfma_stream (gemm_mfma_stream.hip) -- the fast mode for CL a
 //   multiple of 64, whole tiles streamed slab after slab;
-// * chunk_gemm_mfma_kx (gemm_mfma_kx.hip) -- the fast mode for CL = 64 on
-//   GEMMs with few outputs and a long K, a step's chunks spread over waves.
+// * chunk_gemm_mfma_kx, chunk_gemm_mfma_kx16 (gemm_mfma_kx.hip) -- the fast
+//   mode for CL = 64 on GEMMs with few outputs and a long K: a 64 x 64 tile
+//   per 16-wave workgroup, a step's chunks spread over the waves, or (kx16,
+//   the one the planner picks) a 16 x 16 block per wave over the whole K.
 #include <type_traits>
 
 #include "fp8t_device.h"
@@ -245,13 +247,15 @@ constexpr double kP16ProductOps = 6.0;
 // with 64-k slabs, 32 x 32 tiles with 128-k slabs, the streamed 64 x 64
 // kernel and the 64 x 64 kernel with chunks spread over 16 waves (both
 // fitted to their forward and backward-data times; the latter predicts its
-// weight-gradient time within 5%).
+// weight-gradient time within 5%); the 16 x 16 block-per-wave kernel scaled
+// from it by their measured weight-gradient times (0.265 against 0.279 ms).
 double mfma_cost_per_output_chunk(int cfg, int64_t CL) {
-    const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : cfg == 2 ? 0.0856e-9 : 0.0993e-9;
+    const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : cfg == 2 ? 0.0856e-9
+                      : cfg == 3 ? 0.0993e-9 : 0.0942e-9;
     return base * (0.6 + 0.4 * (double)CL / 64.0);
 }
 double mfma_cost_per_tile(int cfg) {
-    return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.67e-6 : 0.93e-6;
+    return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.67e-6 : cfg == 3 ? 0.93e-6 : 0.88e-6;
 }
 
 // VALU_P16: FP16 operands, products rounded to FP16 (chunk_gemm_p16)
@@ -300,7 +304,7 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
             if (mf) {
                 const MfmaShape sh = mfma_shape(cfg);
                 if (CL % sh.kstep != 0) continue;
-                if (cfg == 3 && CL != 64) continue;     // one chunk per wave and step
+                if (cfg >= 3 && CL != 64) continue;     // 64-product chunks only
                 fn = mfma_kernel(cfg, ta, tb);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
                 t_out = mfma_cost_per_output_chunk(cfg, CL);
@@ -386,7 +390,9 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 if (best.cfg < 0 || est < best.est_s) {
                     best.cfg = cfg;
                     best.fn = fn;
-                    best.fn_aligned = mf && cfg == 3 ? mfma_kx_kernel_aligned(ta, tb) : nullptr;
+                    best.fn_aligned = mf && cfg == 3 ? mfma_kx_kernel_aligned(ta, tb)
+                                    : mf && cfg == 4 ? mfma_kx16_kernel_aligned(ta, tb)
+                                                     : nullptr;
                     best.NT = NT;
                     best.BM = BM;
                     best.BN = BN;

@@ -15,7 +15,7 @@ struct MfmaShape {
     int BK;         // k per LDS slab
 };
 
-constexpr int kMfmaConfigs = 4;
+constexpr int kMfmaConfigs = 5;
 
 MfmaShape mfma_shape(int cfg);
 
@@ -33,5 +33,11 @@ const void* mfma_kx_kernel(int ta, int tb);
 // loads of both operands (mfma_kx_aligned): one load path, deeper prefetch.
 bool mfma_kx_aligned(const GemmArgs& g);
 const void* mfma_kx_kernel_aligned(int ta, int tb);
+
+// The same tiles with each of the 16 waves owning a 16 x 16 block over the
+// whole K (gemm_mfma_kx.hip), configuration 4: CL = 64 only, whole tiles
+// only; its aligned variant under the same conditions.
+const void* mfma_kx16_kernel(int ta, int tb);
+const void* mfma_kx16_kernel_aligned(int ta, int tb);
 
 }  // namespace fp8t

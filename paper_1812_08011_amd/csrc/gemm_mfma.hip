@@ -492,6 +492,7 @@ MfmaShape mfma_shape(int cfg) {
         case 0: return MfmaShape{32, 64, 64, kNT, 16, 64};
         case 2: return MfmaShape{32, 64, 64, kNT, 64, 64};      // CL a multiple of 64
         case 3: return MfmaShape{32, 64, 64, 1024, 64, 256};    // CL = 64, 16 waves
+        case 4: return MfmaShape{16, 64, 64, 1024, 64, 256};    // CL = 64, 16 waves
         default: return MfmaShape{16, 32, 32, kNT, 32, 128};
     }
 }
@@ -502,6 +503,7 @@ const void* mfma_kernel(int cfg, int ta, int tb) {
         case 1: return kernel_sel<16, 1, 1, 2, 128>(ta, tb);
         case 2: return mfma_stream_kernel(ta, tb);
         case 3: return mfma_kx_kernel(ta, tb);
+        case 4: return mfma_kx16_kernel(ta, tb);
         default: return nullptr;
     }
 }

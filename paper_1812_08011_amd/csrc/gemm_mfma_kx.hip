@@ -404,6 +404,252 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// The same work cut per wave instead of per chunk: wave w of the workgroup
+// owns the 16 x 16 block (w / 4, w % 4) of the 64 x 64 tile over the whole
+// K, so each output's running sum stays in the registers of the lane that
+// forms it and no chunk sum crosses LDS.  A chunk of 64 products is two
+// v_mfma_f32_16x16x32_bf8_bf8 (k 0..31, then 32..63, accumulated from zero),
+// the instruction sequence of the 16 x 16 block kernel (gemm_mfma.hip), so
+// the bits are that kernel's.  A step's operands (64 rows of A and 64
+// columns of B by 256 k) are staged as above into one of two LDS buffers: the
+// next step's bytes are stored into the other buffer while this step's chunk
+// sums are formed, and one barrier per step orders the two.
+// ---------------------------------------------------------------------------
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <bool TA, bool TB, bool AL>
+__global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4)))
+void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
+    __shared__ __attribute__((aligned(16))) uint8_t As[2][kT][kPitch];
+    __shared__ __attribute__((aligned(16))) uint8_t Bs[2][kT][kPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t Os[kT * kT];
+    __shared__ int redo[kRedoMax];
+    __shared__ int n_redo;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    // the wave's block: rows 16 bi .., columns 16 bj ..; lane l holds operand
+    // row (column) l % 16, k bytes 8 (l / 16) .. +7 of each 32-k instruction,
+    // and results at rows 4 (l / 16) + r, column l % 16 of the block
+    const int bi = wave >> 2, bj = wave & 3;
+    const int arow = 16 * bi + (lane & 15), bcol = 16 * bj + (lane & 15);
+    const int kg = lane >> 4;
+    const int orow = 16 * bi + 4 * kg, ocol = 16 * bj + (lane & 15);
+    if (tid == 0) n_redo = g.guarded ? 0 : kRedoMax + 1;
+
+    StepShare<!TA> sa;             // A is k-contiguous unless transposed
+    StepShare<TB> sb;              // B is k-contiguous only when transposed
+    float S[4];
+    float vmax = 0.0f;
+    const v4f zero = {};
+    const int nch = p.nch;
+    const int nsteps = (nch + kWaves - 1) / kWaves;
+
+    auto tile_origin = [&](int64_t t, int& m0, int& n0) __attribute__((always_inline)) {
+        int tr, tc;
+        tile_rc(p, whole_tile(p, t), tr, tc);
+        m0 = tr * kT;
+        n0 = tc * kT;
+    };
+    auto load = [&](int m0, int n0, int k0) __attribute__((always_inline)) {
+        sa.template load<AL>(g.A, g.lda, m0, g.M, k0, g.K, g.a_vec, g.a_vec16, tid);
+        sb.template load<AL>(g.B, g.ldb, n0, g.N, k0, g.K, g.b_vec, g.b_vec16, tid);
+    };
+    auto store = [&](int buf) __attribute__((always_inline)) {
+        sa.store(As[buf], tid);
+        sb.store(Bs[buf], tid);
+    };
+
+    // The step's chunk sums of the wave's block (chunks past K are not formed).
+    auto chunk_sums = [&](int buf, int s, v4f (&acc)[kWaves]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int c = 0; c < kWaves; ++c) {
+            acc[c] = zero;
+            if (!AL && s * kWaves + c >= nch) continue;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int q = (kCL * c + 32 * h) / 8 + kg;       // 8-byte k slot
+                const long av = *reinterpret_cast<const long*>(&As[buf][arow][slot_off(arow, q)]);
+                const long bv = *reinterpret_cast<const long*>(&Bs[buf][bcol][slot_off(bcol, q)]);
+                acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf8_bf8(av, bv, acc[c], 0, 0, 0);
+            }
+        }
+    };
+    // Each chunk sum rounded to FP16 and added into the running sums, in
+    // chunk order; the guarded path keeps the largest |S| at chunk ends.
+    auto chain = [&](auto safe_tag, int s, const v4f (&acc)[kWaves]) __attribute__((always_inline)) {
+        constexpr bool SAFE = decltype(safe_tag)::value;
+        const int nv = AL ? kWaves : min(kWaves, nch - s * kWaves);
+#pragma unroll
+        for (int c = 0; c < kWaves; ++c) {
+            if (c >= nv) break;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float pr = SAFE ? rn16s(acc[c][r] * 0x1p96f) : rn16v(acc[c][r]);
+                S[r] = SAFE ? rn16s(S[r] + pr) : rn16v(S[r] + pr);
+            }
+            if (!SAFE) {
+                vmax = max3_abs(vmax, S[0], S[1]);
+                vmax = max3_abs(vmax, S[2], S[3]);
+            }
+        }
+    };
+
+    // The finished tile: FP16 codes through Os, 16-byte rows to C (and the
+    // FP8 result to C8).  Os is free: its previous readers finished before
+    // the barrier that ended at least one step since.
+    auto write_tile = [&](auto safe_tag, int m0, int n0) __attribute__((always_inline)) {
+        constexpr int DOM = decltype(safe_tag)::value ? 96 : 0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Os[(orow + r) * kT + ocol] = f32d_to_fp16<DOM>(S[r]);
+        __syncthreads();
+        if (tid < kT * kT / 8) {
+            const int row = tid >> 3, col = (tid & 7) * 8;
+            const int m = m0 + row, n = n0 + col;
+            if (m < g.M) {
+                const uint4 v = *reinterpret_cast<const uint4*>(&Os[row * kT + col]);
+                const uint32_t cw[4] = {v.x, v.y, v.z, v.w};
+                if (g.C) {
+                    uint16_t* cp = g.C + (int64_t)m * g.ldc + n;
+                    if (g.c_vec16 && n + 8 <= g.N) {
+                        *reinterpret_cast<uint4*>(cp) = v;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (n + e < g.N) cp[e] = (uint16_t)(cw[e / 2] >> (16 * (e % 2)));
+                    }
+                }
+                if (g.C8) {
+                    auto val = [&](int e) __attribute__((always_inline)) {
+                        return fp16_to_f32((cw[e / 2] >> (16 * (e % 2))) & 0xFFFFu) * g.q_scale;
+                    };
+                    uint2 v8;
+                    v8.x = f32x2_to_fp8x2<true>(val(2), val(3),
+                                               f32x2_to_fp8x2<false>(val(0), val(1), 0u));
+                    v8.y = f32x2_to_fp8x2<true>(val(6), val(7),
+                                               f32x2_to_fp8x2<false>(val(4), val(5), 0u));
+                    uint8_t* qp = g.C8 + (int64_t)m * g.ldc8 + n;
+                    if (g.c8_vec8 && n + 8 <= g.N) {
+                        *reinterpret_cast<uint2*>(qp) = v8;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            if (n + e < g.N)
+                                qp[e] = (uint8_t)((e < 4 ? v8.x : v8.y) >> (8 * (e % 4)));
+                    }
+                }
+            }
+        }
+    };
+
+    // ---- the stream (guarded epilogue): steps of the workgroup's tiles in
+    // order.  Step cur is consumed from LDS buffer buf while step p1, held in
+    // the registers, is stored into the other buffer and step p2 is loaded
+    // into the registers ----
+    const int64_t T = p.t_whole;
+    struct Pos {
+        int64_t t;                   // work item (tile t of the workgroup's sequence)
+        int s, m0, n0;               // step within the tile, tile origin
+    };
+    auto step_next = [&](Pos& q) __attribute__((always_inline)) {
+        if (++q.s >= nsteps) {
+            q.t += p.G;
+            q.s = 0;
+            if (q.t < T) tile_origin(q.t, q.m0, q.n0);
+        }
+    };
+    if (g.guarded && (int64_t)blockIdx.x < T && nsteps > 0) {
+        Pos cur;
+        cur.t = blockIdx.x;
+        cur.s = 0;
+        tile_origin(cur.t, cur.m0, cur.n0);
+        load(cur.m0, cur.n0, 0);
+        store(0);
+        Pos p1 = cur;
+        step_next(p1);
+        if (p1.t < T) load(p1.m0, p1.n0, p1.s * kSK);
+        __syncthreads();
+        int buf = 0, ordinal = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) S[i] = 0.0f;
+        for (;;) {
+            v4f acc[kWaves];
+            chunk_sums(buf, cur.s, acc);
+            // buffer buf ^ 1 was last read by the previous step, before the
+            // barrier that ended it
+            Pos p2 = p1;
+            if (p1.t < T) {
+                store(buf ^ 1);
+                step_next(p2);
+                if (p2.t < T) load(p2.m0, p2.n0, p2.s * kSK);
+            }
+            chain(std::integral_constant<bool, false>{}, cur.s, acc);
+            if (cur.s + 1 == nsteps) {
+                // tile end: the guard over the whole workgroup (running sums
+                // below 2^31 at every chunk end; NaN from an Inf operand stays
+                // in the running sum and fails the final comparison)
+                bool bad_l = !(vmax < 2147483648.0f);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) bad_l |= !(fabsf(S[i]) < 2147483648.0f);
+                const bool bad = __syncthreads_or(bad_l);
+                if (bad) {
+                    if (tid == 0) {
+                        if (n_redo < kRedoMax) redo[n_redo] = ordinal;
+                        ++n_redo;
+                    }
+                } else {
+                    write_tile(std::integral_constant<bool, false>{}, cur.m0, cur.n0);
+                }
+                vmax = 0.0f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) S[i] = 0.0f;
+                ++ordinal;
+            }
+            if (p1.t >= T) break;
+            __syncthreads();                     // buf read, buf ^ 1 written
+            buf ^= 1;
+            cur = p1;
+            p1 = p2;
+        }
+    }
+
+    // ---- tiles that failed the guard (all of them when it is off, or when
+    // more failed than the list holds), recomputed in the 2^96 domain ----
+    __syncthreads();
+    const int nr = n_redo;
+    if (nr == 0 || nsteps == 0) return;
+    int ord = 0, next_listed = 0;
+    for (int64_t u = blockIdx.x; u < T; u += p.G, ++ord) {
+        const bool listed = nr > kRedoMax || (next_listed < nr && redo[next_listed] == ord);
+        if (!listed) continue;
+        if (nr <= kRedoMax) ++next_listed;
+        int m0, n0;
+        tile_origin(u, m0, n0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) S[i] = 0.0f;
+        for (int s = 0; s < nsteps; ++s) {
+            load(m0, n0, s * kSK);
+            __syncthreads();                     // buffer 0 read by the previous step
+            store(0);
+            __syncthreads();
+            v4f acc[kWaves];
+            chunk_sums(0, s, acc);
+            chain(std::integral_constant<bool, true>{}, s, acc);
+        }
+        __syncthreads();                         // Os readers of the previous tile are done
+        write_tile(std::integral_constant<bool, true>{}, m0, n0);
+    }
+}
+
+template <bool AL>
+const void* kx16_sel(int ta, int tb) {
+    if (!ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma_kx16<false, false, AL>);
+    if (!ta && tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma_kx16<false, true, AL>);
+    if (ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma_kx16<true, false, AL>);
+    return reinterpret_cast<const void*>(&chunk_gemm_mfma_kx16<true, true, AL>);
+}
+
 template <bool AL>
 const void* kx_sel(int ta, int tb) {
     if (!ta && !tb) return reinterpret_cast<const void*>(&chunk_gemm_mfma_kx<false, false, AL>);
@@ -421,5 +667,9 @@ bool mfma_kx_aligned(const GemmArgs& g) {
 }
 
 const void* mfma_kx_kernel_aligned(int ta, int tb) { return kx_sel<true>(ta, tb); }
+
+const void* mfma_kx16_kernel(int ta, int tb) { return kx16_sel<false>(ta, tb); }
+
+const void* mfma_kx16_kernel_aligned(int ta, int tb) { return kx16_sel<true>(ta, tb); }
 
 }  // namespace fp8t

@@ -309,7 +309,7 @@ def test_chunk_gemm_workspace_contract():
         assert np.array_equal(host(C), Co)
 
 
-@pytest.mark.parametrize("mtile", ["auto", "0", "1", "2", "3"])
+@pytest.mark.parametrize("mtile", ["auto", "0", "1", "2", "3", "4"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
     """Fast mode against the fast oracle within the derived tolerance, for
@@ -389,7 +389,7 @@ def test_chunk_gemm_fast_shared_tiles(mtile, wgs, ta, tb, monkeypatch):
 
 
 @pytest.mark.parametrize("mtile,split", [("0", "0"), ("1", "0"), ("2", "0"), ("3", "0"),
-                                         ("0", "1"), ("1", "1")])
+                                         ("4", "0"), ("0", "1"), ("1", "1")])
 def test_chunk_gemm_fast_specials(mtile, split, monkeypatch):
     """Inf and NaN operands through every matrix-core kernel, in whole tiles
     and in the later pieces of shared tiles (chunk sums through the
@@ -485,6 +485,70 @@ def test_chunk_gemm_fast_chunks_over_waves_same_bits(ta, tb, monkeypatch):
         vb = oracle.p8_value(B.T if tb else B)
         check_fast(got["30", "1"], A, B, 64, ta, tb, f"fast kx {M}x{N}x{K}", Co=Co,
                    absum=abs_dot(va, vb), K=K)
+
+
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_chunk_gemm_fast_block_per_wave_same_bits(ta, tb, monkeypatch):
+    """The 64 x 64-tile kernel whose 16 waves each own a 16 x 16 block over
+    the whole K (CL = 64) forms every chunk sum with the instruction sequence
+    of the 16 x 16 block kernel (two 16x16x32 steps from zero) and adds them
+    in the same order, so the two give the same bits: ragged M, N and K,
+    padded leading dimensions and misaligned bases, several tiles per
+    workgroup, both epilogues, tiles failing the overflow guard, the FP8
+    result in the same pass; and the fast oracle's bounds hold."""
+    rng = np.random.default_rng(600 + 2 * ta + tb)
+    cases = [(32, 32, 64, 0, 0), (33, 31, 65, 0, 0), (100, 70, 64 * 9 + 17, 0, 0),
+             (64, 96, 64 * 14, 0, 0), (70, 45, 64 * 23 + 40, 5, 1), (40, 72, 64 * 6, 3, 3),
+             (128, 64, 1024, 0, 0), (64, 128, 768, 0, 0), (128, 192, 512, 0, 0)]
+    for ci, (M, N, K, pad, off) in enumerate(cases):
+        A, B = _operands(rng, M, N, K, ta, tb)
+        if ci == len(cases) - 1:
+            (A.T if ta else A)[37, :] = 0x7B                     # 57344
+            (B if tb else B.T)[70, :] = np.where(rng.random(K) < 0.5, 0x7A, 0xFA)
+        if ci == 4:
+            (A.T if ta else A)[3, 70] = 0x7C                     # +Inf
+            (B if tb else B.T)[9, 1000] = 0x7D                   # NaN
+        lda, ldb = A.shape[1] + pad, B.shape[1] + pad
+        Ap = np.zeros((A.shape[0], lda), np.uint8)
+        Bp = np.zeros((B.shape[0], ldb), np.uint8)
+        Ap[:, :A.shape[1]] = A
+        Bp[:, :B.shape[1]] = B
+        Ad = dev(np.concatenate([np.zeros(off, np.uint8), Ap.ravel()]))[off:]
+        Bd = dev(np.concatenate([np.zeros(off, np.uint8), Bp.ravel()]))[off:]
+        got = {}
+        for mtile, wgs in (("1", "0"), ("4", "0"), ("4", "3")):
+            monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
+            monkeypatch.setenv("FP8T_GEMM_WGS", wgs)     # 3: several tiles per workgroup
+            for guard in ("1", "0"):
+                monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+                say(f"fast block per wave mtile={mtile} wgs={wgs} guard={guard} ta={ta} "
+                    f"tb={tb} {M}x{N}x{K} pad={pad} off={off}")
+                got[mtile + wgs, guard] = host(gemm(Ad, Bd, M, N, K, 64, ta, tb,
+                                                    mode=fp8t.FAST, lda=lda, ldb=ldb))
+        monkeypatch.delenv("FP8T_GEMM_WGS")
+        ref = got["10", "1"]
+        for key, C in got.items():
+            assert np.array_equal(C, ref), (key, M, N, K, np.argwhere(C != ref)[:5])
+        monkeypatch.setenv("FP8T_GEMM_GUARD", "1")
+        monkeypatch.setenv("FP8T_MFMA_TILE", "4")
+        for with_c in (True, False):
+            C8 = torch.full((M, N + 3), 0xEE, dtype=torch.uint8, device=DEV)
+            C = torch.empty((M, N), dtype=torch.uint16, device=DEV) if with_c else None
+            ws_b = fp8t.chunk_gemm_fp8_workspace_size(ta, tb, M, N, K, 64, fp8t.FAST)
+            ws = torch.empty(max(ws_b, 1), dtype=torch.uint8, device=DEV)
+            fp8t.chunk_gemm_fp8(ta, tb, M, N, K, 64, Ad, lda, Bd, ldb, C, N, C8, N + 3,
+                                0.5, fp8t.FAST, ws, ws_b)
+            q8 = host(C8)
+            assert np.all(q8[:, N:] == 0xEE)
+            assert np.array_equal(q8[:, :N], oracle.fp8_quantize(ref, 0.5))
+            if with_c:
+                assert np.array_equal(host(C), ref)
+        if ci != 4:
+            Co = oracle.chunk_gemm(A, B, 64, ta, tb, mode=oracle.FAST)
+            va = oracle.p8_value(A.T if ta else A)
+            vb = oracle.p8_value(B.T if tb else B)
+            check_fast(got["40", "1"], A, B, 64, ta, tb, f"fast kx16 {M}x{N}x{K}", Co=Co,
+                       absum=abs_dot(va, vb), K=K)
 
 
 def test_chunk_gemm_padded_leading_dims_and_misaligned_bases():
@@ -611,7 +675,7 @@ def test_chunk_gemm_guard_threshold(b0, CL, tile, monkeypatch):
             assert np.array_equal(Cg, Co), np.argwhere(Cg != Co)[:5]
 
 
-@pytest.mark.parametrize("mtile", ["0", "1", "2", "3"])
+@pytest.mark.parametrize("mtile", ["0", "1", "2", "3", "4"])
 @pytest.mark.parametrize("wgs", ["0", "1"])
 def test_chunk_gemm_fast_guard_falls_back(mtile, wgs, monkeypatch):
     """Fast mode: pieces whose chunk sums reach 2^32 are recomputed on the
