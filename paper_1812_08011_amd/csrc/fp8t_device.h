@@ -106,6 +106,21 @@ __device__ __forceinline__ uint16_t f32d_to_fp16(float x) {
     return (uint16_t)(s | k);
 }
 
+// FP16 code of a plain value that is already on the FP16 grid and below
+// 2^32 in magnitude -- what the exact mode's guarded path holds; a piece in
+// which a value left that range fails the guard and is recomputed on the
+// safe path, which overwrites whatever this wrote.  Normal values (from
+// 2^-30) by moving the fields, subnormal ones (m 2^-39) by scaling m back to
+// an integer: the same codes as f32d_to_fp16<0> in that range, without its
+// Inf/NaN/overflow cases.
+__device__ __forceinline__ uint16_t f32g_to_fp16(float x) {
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t a = u & 0x7FFFFFFFu;
+    const uint32_t n = (a >> 14) - (96u << 9);
+    const uint32_t k = (uint32_t)(__uint_as_float(a) * 0x1p39f);
+    return (uint16_t)(((u >> 16) & 0x8000u) | (a >= (97u << 23) ? n : k));
+}
+
 // Round to a 10-bit significand, ties to even, by Veltkamp splitting
 // (c = x (2^14 + 1), hi = c - (c - x)): three full-rate VALU operations.
 // Valid when x (2^14 + 1) neither overflows nor leaves the normal range --

@@ -518,6 +518,13 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 #pragma unroll
             for (int j = 0; j < TN; ++j) { P[i][j] = 0.0f; S[i][j] = 0.0f; }
 
+        // FP16 code of a chunk sum or running sum: on the guarded path the
+        // value is on the FP16 grid and, unless the piece fails its guard
+        // (and is redone on the safe path), below 2^32
+        auto code = [&](float x) __attribute__((always_inline)) -> uint32_t {
+            if constexpr (!SAFE && !FAST) return f32g_to_fp16(x);
+            else return f32d_to_fp16<DOM>(x);
+        };
         auto flush = [&]() __attribute__((always_inline)) {
             if (to_ws) {
 #pragma unroll
@@ -526,9 +533,9 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                     uint32_t w[(TN + 1) / 2];
 #pragma unroll
                     for (int j = 0; j < TN; j += 2) {
-                        uint32_t c = f32d_to_fp16<DOM>(chunk_value(P[i][j]));
+                        uint32_t c = code(chunk_value(P[i][j]));
                         if (j + 1 < TN)
-                            c |= (uint32_t)f32d_to_fp16<DOM>(chunk_value(P[i][j + 1])) << 16;
+                            c |= code(chunk_value(P[i][j + 1])) << 16;
                         w[j / 2] = c;
                     }
                     if (TN == 1) {
@@ -690,7 +697,7 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) dst[i * BN + j] = f32d_to_fp16<DOM>(S[i][j]);
+                for (int j = 0; j < TN; ++j) dst[i * BN + j] = (uint16_t)code(S[i][j]);
             return true;
         }
         // The running sum: a lane's TN consecutive codes of a row are stored
@@ -710,23 +717,23 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
 #pragma unroll
                     for (int j = 0; j < TN; j += 4) {
                         uint2 c;
-                        c.x = (uint32_t)f32d_to_fp16<DOM>(S[i][j]) |
-                              ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 1]) << 16);
-                        c.y = (uint32_t)f32d_to_fp16<DOM>(S[i][j + 2]) |
-                              ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 3]) << 16);
+                        c.x = code(S[i][j]) |
+                              (code(S[i][j + 1]) << 16);
+                        c.y = code(S[i][j + 2]) |
+                              (code(S[i][j + 3]) << 16);
                         reinterpret_cast<uint2*>(crow)[j / 4] = c;
                     }
                 } else if (TN > 1 && g.c_vec && nl + TN <= g.N) {
 #pragma unroll
                     for (int j = 0; j < TN; j += 2) {
-                        uint32_t c = (uint32_t)f32d_to_fp16<DOM>(S[i][j]) |
-                                     ((uint32_t)f32d_to_fp16<DOM>(S[i][j + 1]) << 16);
+                        uint32_t c = code(S[i][j]) |
+                                     (code(S[i][j + 1]) << 16);
                         reinterpret_cast<uint32_t*>(crow)[j / 2] = c;
                     }
                 } else {
 #pragma unroll
                     for (int j = 0; j < TN; ++j)
-                        if (nl + j < g.N) crow[j] = f32d_to_fp16<DOM>(S[i][j]);
+                        if (nl + j < g.N) crow[j] = (uint16_t)code(S[i][j]);
                 }
             }
             if (g.C8 && lt < 0) {
