@@ -121,6 +121,15 @@ __device__ __forceinline__ uint16_t f32g_to_fp16(float x) {
     return (uint16_t)(((u >> 16) & 0x8000u) | (a >= (97u << 23) ? n : k));
 }
 
+// FP16 code of a GEMM result in the domain scaled by 2^DOM: 0 is the
+// guarded epilogues' plain domain, whose values are on the FP16 grid and
+// below 2^32 wherever they are kept (f32g_to_fp16), 96 the safe path's.
+template <int DOM>
+__device__ __forceinline__ uint16_t fp16_code(float x) {
+    if constexpr (DOM == 0) return f32g_to_fp16(x);
+    else return f32d_to_fp16<DOM>(x);
+}
+
 // Round to a 10-bit significand, ties to even, by Veltkamp splitting
 // (c = x (2^14 + 1), hi = c - (c - x)): three full-rate VALU operations.
 // Valid when x (2^14 + 1) neither overflows nor leaves the normal range --

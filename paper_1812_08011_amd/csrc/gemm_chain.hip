@@ -256,7 +256,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_chain(GemmArgs g, Plan p) {
             for (int j = 0; j < TN; ++j) {
                 const int n = n0 + lx + 16 * j;
                 if (n >= g.N) continue;
-                if (g.C) g.C[(int64_t)m * g.ldc + n] = f32d_to_fp16<DOM>(S[i][j]);
+                if (g.C) g.C[(int64_t)m * g.ldc + n] = fp16_code<DOM>(S[i][j]);
                 if (g.C8)
                     g.C8[(int64_t)m * g.ldc8 + n] =
                         (uint8_t)f32d_to_fp8_scaled<DOM>(S[i][j], g.q_scale);

@@ -266,7 +266,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                             nonfinite |= !(fabsf(pv) < 2147483648.0f);
                         }
                         g.ws[ws_index(p, BM, BN, lt, chunk, r0 + I::out_row(lane, r), c)] =
-                            f32d_to_fp16<DOM>(pv);
+                            fp16_code<DOM>(pv);
                         acc[i][j][r] = 0.0f;
                     }
                 }
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
 #pragma unroll
                 for (int r = 0; r < NR; ++r)
                     ot[(wy * FM * BW + i * BW + I::out_row(lane, r)) * BN + wx * FN * BW +
-                       j * BW + I::out_col(lane)] = f32d_to_fp16<DOM>(S[i][j][r]);
+                       j * BW + I::out_col(lane)] = fp16_code<DOM>(S[i][j][r]);
         __syncthreads();
         const bool keep = lt >= 0 && !g.C;
         for (int u = tid; u < BM * BN / 8; u += kNT) {

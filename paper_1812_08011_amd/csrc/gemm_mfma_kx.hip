@@ -252,7 +252,7 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int l = sl + i;
-            Os[(orow0 + res_row(l, sr)) * kT + ocol0 + (l & 31)] = f32d_to_fp16<DOM>(S[i]);
+            Os[(orow0 + res_row(l, sr)) * kT + ocol0 + (l & 31)] = fp16_code<DOM>(S[i]);
         }
         __syncthreads();
         if (tid < kT * kT / 8) {
@@ -502,7 +502,7 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
     auto write_tile = [&](auto safe_tag, int m0, int n0) __attribute__((always_inline)) {
         constexpr int DOM = decltype(safe_tag)::value ? 96 : 0;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Os[(orow + r) * kT + ocol] = f32d_to_fp16<DOM>(S[r]);
+        for (int r = 0; r < 4; ++r) Os[(orow + r) * kT + ocol] = fp16_code<DOM>(S[r]);
         __syncthreads();
         if (tid < kT * kT / 8) {
             const int row = tid >> 3, col = (tid & 7) * 8;

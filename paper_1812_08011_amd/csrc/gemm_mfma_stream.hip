@@ -226,7 +226,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                     nonfinite |= !(fabsf(pv) < 2147483648.0f);
                 }
                 g.ws[ws_index(p, kB, kB, it.lt, chunk, wy * 32 + out_row(lane, r), bcol)] =
-                    f32d_to_fp16<DOM>(pv);
+                    fp16_code<DOM>(pv);
             }
         } else {
 #pragma unroll
@@ -284,7 +284,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
         geom(it, m0, n0, kbeg, kend);
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-            Os[(wy * 32 + out_row(lane, r)) * kB + bcol] = f32d_to_fp16<DOM>(S[r]);
+            Os[(wy * 32 + out_row(lane, r)) * kB + bcol] = fp16_code<DOM>(S[r]);
         __syncthreads();
         const bool keep = it.lt >= 0 && !g.C;
 #pragma unroll
