@@ -7,6 +7,23 @@
 
 namespace fp8t {
 
+// Workgroup-wide OR of one flag per thread with a single barrier (the fast
+// kernels' guard vote at a piece end; __syncthreads_or took three barriers
+// and a load of the workgroup size): each wave votes, one lane of a wave
+// with a set flag writes 1 into slots[s] (all writers write the same value),
+// thread 0 clears the other slot for the next vote, and after the barrier
+// every thread reads slots[s]; s alternates.  Both slots start at 0, and a
+// caller has at least one barrier between two votes, so the readers of the
+// other slot's previous vote are past it when thread 0 clears it.
+__device__ __forceinline__ bool block_any(bool flag, uint32_t* slots, int& s) {
+    if (__any(flag) && (threadIdx.x & 63) == 0) slots[s] = 1u;
+    if (threadIdx.x == 0) slots[s ^ 1] = 0u;
+    __syncthreads();
+    const bool r = slots[s] != 0u;
+    s ^= 1;
+    return r;
+}
+
 struct MfmaShape {
     int BW;         // MFMA block (32: 32x32x16, 16: 16x16x32)
     int BM, BN;     // outputs per workgroup

@@ -185,10 +185,13 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
 
     __shared__ __attribute__((aligned(16))) uint8_t As[2][BM][kPitch];
     __shared__ __attribute__((aligned(16))) uint8_t Bs[2][BN][kPitch];
+    __shared__ uint32_t s_vote[2];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int wy = wave >> 1, wx = wave & 1;
+    if (tid == 0) s_vote[0] = s_vote[1] = 0u;     // ordered by the first slab's barrier
+    int vslot = 0;
 
     Slab<!TA, BM, kBK> la[kStages];      // A is k-contiguous unless transposed
     Slab<TB, BN, kBK> lb[kStages];       // B is k-contiguous only when transposed
@@ -386,7 +389,7 @@ __global__ __launch_bounds__(kNT) void chunk_gemm_mfma(GemmArgs g, Plan p) {
                 for (int j = 0; j < FN; ++j)
 #pragma unroll
                     for (int r = 0; r < NR; ++r) bad |= !(fabsf(S[i][j][r]) < 2147483648.0f);
-            if (__syncthreads_or(bad)) return false;
+            if (block_any(bad, s_vote, vslot)) return false;
         }
         if (to_ws) return true;
         // Results leave through LDS (free after the last slab's barrier): the

@@ -151,6 +151,7 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
     __shared__ __attribute__((aligned(16))) uint16_t Os[kT * kT];
     __shared__ int redo[kRedoMax];
     __shared__ int n_redo;
+    __shared__ uint32_t s_vote[2];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -163,7 +164,11 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
     const int cq = tid >> 8, u = tid & 255;
     const int sr = u >> 4, sl = 4 * (u & 15);
     const int orow0 = 32 * (cq >> 1), ocol0 = 32 * (cq & 1);
-    if (tid == 0) n_redo = g.guarded ? 0 : kRedoMax + 1;
+    if (tid == 0) {
+        n_redo = g.guarded ? 0 : kRedoMax + 1;
+        s_vote[0] = s_vote[1] = 0u;
+    }
+    int vslot = 0;
 
     StepShare<!TA> sa[2];          // A is k-contiguous unless transposed
     StepShare<TB> sb[2];           // B is k-contiguous only when transposed
@@ -348,7 +353,7 @@ void chunk_gemm_mfma_kx(GemmArgs g, Plan p) {
                 bool bad_l = !(vmax < 2147483648.0f);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) bad_l |= !(fabsf(S[i]) < 2147483648.0f);
-                const bool bad = __syncthreads_or(bad_l);
+                const bool bad = block_any(bad_l, s_vote, vslot);
                 if (bad) {
                     if (tid == 0) {
                         if (n_redo < kRedoMax) redo[n_redo] = ordinal;
@@ -426,6 +431,7 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
     __shared__ __attribute__((aligned(16))) uint16_t Os[kT * kT];
     __shared__ int redo[kRedoMax];
     __shared__ int n_redo;
+    __shared__ uint32_t s_vote[2];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -436,7 +442,11 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
     const int arow = 16 * bi + (lane & 15), bcol = 16 * bj + (lane & 15);
     const int kg = lane >> 4;
     const int orow = 16 * bi + 4 * kg, ocol = 16 * bj + (lane & 15);
-    if (tid == 0) n_redo = g.guarded ? 0 : kRedoMax + 1;
+    if (tid == 0) {
+        n_redo = g.guarded ? 0 : kRedoMax + 1;
+        s_vote[0] = s_vote[1] = 0u;
+    }
+    int vslot = 0;
 
     StepShare<!TA> sa;             // A is k-contiguous unless transposed
     StepShare<TB> sb;              // B is k-contiguous only when transposed
@@ -592,7 +602,7 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
                 bool bad_l = !(vmax < 2147483648.0f);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) bad_l |= !(fabsf(S[i]) < 2147483648.0f);
-                const bool bad = __syncthreads_or(bad_l);
+                const bool bad = block_any(bad_l, s_vote, vslot);
                 if (bad) {
                     if (tid == 0) {
                         if (n_redo < kRedoMax) redo[n_redo] = ordinal;

@@ -176,6 +176,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
     __shared__ __attribute__((aligned(16))) uint16_t Os[kB * kB];
     __shared__ int redo[kRedoMax];
     __shared__ int n_redo;
+    __shared__ uint32_t s_vote[2];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -183,7 +184,11 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
     const int arow = wy * 32 + (lane & 31), bcol = wx * 32 + (lane & 31);
     const int kq = 32 * (lane >> 5);
     // with the guarded epilogue switched off every piece takes the safe one
-    if (tid == 0) n_redo = g.guarded ? 0 : kRedoMax + 1;
+    if (tid == 0) {
+        n_redo = g.guarded ? 0 : kRedoMax + 1;
+        s_vote[0] = s_vote[1] = 0u;
+    }
+    int vslot = 0;
 
     Share<!TA> sa;                 // A is k-contiguous unless transposed
     Share<TB> sb;                  // B is k-contiguous only when transposed
@@ -371,7 +376,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                 bool bad_l = !(vmax < 2147483648.0f) || nonfinite;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) bad_l |= !(fabsf(S[r]) < 2147483648.0f);
-                const bool bad = __syncthreads_or(bad_l);
+                const bool bad = block_any(bad_l, s_vote, vslot);
                 if (bad) {
                     if (tid == 0) {
                         if (n_redo < kRedoMax) redo[n_redo] = ordinal;
