@@ -112,20 +112,22 @@ __device__ __forceinline__ uint16_t f32d_to_fp16(float x) {
 // safe path, which overwrites whatever this wrote.  Normal values (from
 // 2^-30) by moving the fields, subnormal ones (m 2^-39) by scaling m back to
 // an integer: the same codes as f32d_to_fp16<0> in that range, without its
-// Inf/NaN/overflow cases.
-__device__ __forceinline__ uint16_t f32g_to_fp16(float x) {
+// Inf/NaN/overflow cases.  The code comes in the low 16 bits of a 32-bit
+// word whose upper bits are zero in that range (callers pack two codes
+// without masking).
+__device__ __forceinline__ uint32_t f32g_to_fp16(float x) {
     const uint32_t u = __float_as_uint(x);
     const uint32_t a = u & 0x7FFFFFFFu;
     const uint32_t n = (a >> 14) - (96u << 9);
     const uint32_t k = (uint32_t)(__uint_as_float(a) * 0x1p39f);
-    return (uint16_t)(((u >> 16) & 0x8000u) | (a >= (97u << 23) ? n : k));
+    return ((u >> 16) & 0x8000u) | (a >= (97u << 23) ? n : k);
 }
 
 // FP16 code of a GEMM result in the domain scaled by 2^DOM: 0 is the
 // guarded epilogues' plain domain, whose values are on the FP16 grid and
 // below 2^32 wherever they are kept (f32g_to_fp16), 96 the safe path's.
 template <int DOM>
-__device__ __forceinline__ uint16_t fp16_code(float x) {
+__device__ __forceinline__ uint32_t fp16_code(float x) {
     if constexpr (DOM == 0) return f32g_to_fp16(x);
     else return f32d_to_fp16<DOM>(x);
 }
