@@ -50,7 +50,7 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 300.0 MB, weight-gradient 2402.6 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "b4cd871aeaf099474392724e9c8a4c66cc9b3b0a8ea819124120e31809aa3f0d"
+TRAFFIC_SOURCES_SHA256 = "84979dcd8658e981b9b6abaff202aa91355a0d75a6ef06152e006e6015e52c2c"
 EXACT_TRAFFIC_BYTES_PER_CALL = 964.4e6
 
 
