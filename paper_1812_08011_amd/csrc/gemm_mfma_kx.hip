@@ -509,11 +509,14 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
     // The finished tile: FP16 codes through Os, 16-byte rows to C (and the
     // FP8 result to C8).  Os is free: its previous readers finished before
     // the barrier that ended at least one step since.
-    auto write_tile = [&](auto safe_tag, int m0, int n0) __attribute__((always_inline)) {
+    // (staging the codes and storing them from Os are split so that the
+    // guarded stream's tile-end vote barrier orders the two)
+    auto stage_tile = [&](auto safe_tag) __attribute__((always_inline)) {
         constexpr int DOM = decltype(safe_tag)::value ? 96 : 0;
 #pragma unroll
         for (int r = 0; r < 4; ++r) Os[(orow + r) * kT + ocol] = fp16_code<DOM>(S[r]);
-        __syncthreads();
+    };
+    auto store_tile = [&](int m0, int n0) __attribute__((always_inline)) {
         if (tid < kT * kT / 8) {
             const int row = tid >> 3, col = (tid & 7) * 8;
             const int m = m0 + row, n = n0 + col;
@@ -551,6 +554,11 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
                 }
             }
         }
+    };
+    auto write_tile = [&](auto safe_tag, int m0, int n0) __attribute__((always_inline)) {
+        stage_tile(safe_tag);
+        __syncthreads();
+        store_tile(m0, n0);
     };
 
     // ---- the stream (guarded epilogue): steps of the workgroup's tiles in
@@ -602,6 +610,9 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
                 bool bad_l = !(vmax < 2147483648.0f);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) bad_l |= !(fabsf(S[i]) < 2147483648.0f);
+                // the codes go to Os before the vote (a failed tile's are
+                // never stored), whose barrier then orders them for the stores
+                stage_tile(std::integral_constant<bool, false>{});
                 const bool bad = block_any(bad_l, s_vote, vslot);
                 if (bad) {
                     if (tid == 0) {
@@ -609,7 +620,7 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
                         ++n_redo;
                     }
                 } else {
-                    write_tile(std::integral_constant<bool, false>{}, cur.m0, cur.n0);
+                    store_tile(cur.m0, cur.n0);
                 }
                 vmax = 0.0f;
 #pragma unroll

@@ -283,14 +283,17 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
 
     // Piece end: results of a piece that starts its tile (the running sums:
     // C / C8 for a whole tile, C or s_ws for the first piece of a split tile).
-    auto write_sums = [&](auto safe_tag, const Item& it) __attribute__((always_inline)) {
+    // Staging the codes and storing them from Os are split so that the
+    // guarded stream's piece-end vote barrier orders the two.
+    auto stage_sums = [&](auto safe_tag) __attribute__((always_inline)) {
         constexpr int DOM = decltype(safe_tag)::value ? 96 : 0;
-        int m0, n0, kbeg, kend;
-        geom(it, m0, n0, kbeg, kend);
 #pragma unroll
         for (int r = 0; r < 16; ++r)
             Os[(wy * 32 + out_row(lane, r)) * kB + bcol] = fp16_code<DOM>(S[r]);
-        __syncthreads();
+    };
+    auto store_sums = [&](const Item& it) __attribute__((always_inline)) {
+        int m0, n0, kbeg, kend;
+        geom(it, m0, n0, kbeg, kend);
         const bool keep = it.lt >= 0 && !g.C;
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
@@ -331,7 +334,12 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                 }
             }
         }
-        // Os is next written after the barrier that ends the next piece
+        // Os is next written after at least one more barrier
+    };
+    auto write_sums = [&](auto safe_tag, const Item& it) __attribute__((always_inline)) {
+        stage_sums(safe_tag);
+        __syncthreads();
+        store_sums(it);
     };
 
     // ---- the stream (guarded epilogue) ----
@@ -376,6 +384,9 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                 bool bad_l = !(vmax < 2147483648.0f) || nonfinite;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) bad_l |= !(fabsf(S[r]) < 2147483648.0f);
+                // the codes go to Os before the vote (a failed piece's are
+                // never stored), whose barrier then orders them for the stores
+                if (cur.it.c0 == 0) stage_sums(std::integral_constant<bool, false>{});
                 const bool bad = block_any(bad_l, s_vote, vslot);
                 if (bad) {
                     if (tid == 0) {
@@ -383,7 +394,7 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
                         ++n_redo;
                     }
                 } else if (cur.it.c0 == 0) {
-                    write_sums(std::integral_constant<bool, false>{}, cur.it);
+                    store_sums(cur.it);
                 }
                 vmax = 0.0f;
                 nonfinite = false;
