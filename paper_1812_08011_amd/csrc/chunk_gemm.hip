@@ -88,6 +88,19 @@ static_assert(kFoldV == 2 || kFoldV == 4 || kFoldV == 8, "2, 4 or 8 outputs per 
 typedef std::conditional<kFoldV == 8, uint4,
                          std::conditional<kFoldV == 4, uint2, uint32_t>::type>::type FoldVec;
 
+// A workspace vector loaded non-temporally (each chunk sum is read once).
+__device__ __forceinline__ uint32_t nt_load(const uint32_t* q) { return __builtin_nontemporal_load(q); }
+__device__ __forceinline__ uint2 nt_load(const uint2* q) {
+    typedef uint32_t v2 __attribute__((ext_vector_type(2)));
+    const v2 v = __builtin_nontemporal_load(reinterpret_cast<const v2*>(q));
+    return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ uint4 nt_load(const uint4* q) {
+    typedef uint32_t v4 __attribute__((ext_vector_type(4)));
+    const v4 v = __builtin_nontemporal_load(reinterpret_cast<const v4*>(q));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __global__ __launch_bounds__(kFoldT) void chunk_fold(GemmArgs g, Plan p, int BM, int BN) {
     const int64_t per = (int64_t)BM * BN;
     const int64_t idx = ((int64_t)blockIdx.x * kFoldT + threadIdx.x) * kFoldV;
@@ -133,7 +146,7 @@ __global__ __launch_bounds__(kFoldT) void chunk_fold(GemmArgs g, Plan p, int BM,
         if (c0 + kFoldU <= p.nch) {
             const FoldVec* b = src + (int64_t)c0 * step;
 #pragma unroll
-            for (int u = 0; u < kFoldU; ++u) q[u] = b[u * step];
+            for (int u = 0; u < kFoldU; ++u) q[u] = nt_load(&b[u * step]);
         } else {
 #pragma unroll
             for (int u = 0; u < kFoldU; ++u) q[u] = src[(int64_t)min(c0 + u, last) * step];

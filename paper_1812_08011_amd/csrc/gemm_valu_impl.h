@@ -538,7 +538,14 @@ void chunk_gemm_valu(GemmArgs g, Plan p) {
                             c |= code(chunk_value(P[i][j + 1])) << 16;
                         w[j / 2] = c;
                     }
-                    if (TN == 1) {
+                    // chunk sums are read once, by the fold pass: stored
+                    // non-temporally (4 codes per store where the lane has
+                    // them), so they do not evict the operands' lines
+                    if constexpr (TN == 4) {
+                        typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+                        const u32x2_t v = {w[0], w[1]};
+                        __builtin_nontemporal_store(v, reinterpret_cast<u32x2_t*>(dst));
+                    } else if (TN == 1) {
                         dst[0] = (uint16_t)w[0];
                     } else {
 #pragma unroll
