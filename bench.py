@@ -50,8 +50,8 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 300.0 MB, weight-gradient 2402.6 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "84979dcd8658e981b9b6abaff202aa91355a0d75a6ef06152e006e6015e52c2c"
-EXACT_TRAFFIC_BYTES_PER_CALL = 964.4e6
+TRAFFIC_SOURCES_SHA256 = "e55505c8e3cc11e93b78e7fa2668577f7a68848be37233870b356556335592d0"
+EXACT_TRAFFIC_BYTES_PER_CALL = 963.8e6
 
 
 # The sources that decide what an exact-mode chunk_gemm call runs: the VALU
