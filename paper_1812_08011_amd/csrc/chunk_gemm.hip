@@ -261,15 +261,27 @@ constexpr double kP16ProductOps = 6.0;
 // kernel and the 64 x 64 kernel with chunks spread over 16 waves (both
 // fitted to their forward and backward-data times; the latter predicts its
 // weight-gradient time within 5%); the 16 x 16 block-per-wave kernel scaled
-// from it by their measured weight-gradient times (0.265 against 0.279 ms).
+// from it by their measured weight-gradient times (0.265 against 0.279 ms);
+// the wave-independent 32 x 128 kernel fitted to its forward and
+// backward-data times (one tile per workgroup).
 double mfma_cost_per_output_chunk(int cfg, int64_t CL) {
     const double base = cfg == 0 ? 0.156e-9 : cfg == 1 ? 0.17e-9 : cfg == 2 ? 0.0856e-9
-                      : cfg == 3 ? 0.0993e-9 : 0.0942e-9;
+                      : cfg == 3 ? 0.0993e-9 : cfg == 4 ? 0.0942e-9 : 0.0557e-9;
     return base * (0.6 + 0.4 * (double)CL / 64.0);
 }
 double mfma_cost_per_tile(int cfg) {
-    return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.67e-6 : cfg == 3 ? 0.93e-6 : 0.88e-6;
+    return cfg == 0 ? 1.1e-6 : cfg == 1 ? 0.66e-6 : cfg == 2 ? 0.67e-6 : cfg == 3 ? 0.93e-6
+         : cfg == 4 ? 0.88e-6 : 0.33e-6;
 }
+constexpr size_t kWsAlignBt = 256;
+
+// The k-contiguous copy of an operand B stored with n contiguous (the
+// wave-independent kernel's second operand): its workspace bytes, and its
+// cost (one small kernel reading and writing N x K bytes).
+size_t wave_bt_bytes(int64_t N, int64_t K) {
+    return (size_t)N * (size_t)((K + 15) / 16 * 16) + kWsAlignBt;
+}
+double wave_bt_cost(int64_t N, int64_t K) { return 2e-6 + 2.0 * (double)N * (double)K / 3e12; }
 
 // VALU_P16: FP16 operands, products rounded to FP16 (chunk_gemm_p16)
 enum Kind { VALU_EXACT = 0, VALU_FAST = 1, MFMA_FAST = 2, VALU_P16 = 3 };
@@ -280,7 +292,8 @@ struct Choice {
     const void* fn_aligned = nullptr;    // variant taken when mfma_kx_aligned(args)
     int NT = 0, BM = 0, BN = 0;
     Plan plan{};
-    size_t ws_bytes = 0;
+    size_t ws_bytes = 0;                 // chunk sums of the shared tiles
+    size_t bt_bytes = 0;                 // the k-contiguous copy of B (configuration 5)
     double est_s = 0.0;
 };
 
@@ -288,9 +301,11 @@ constexpr size_t kWsAlign = 256;
 
 // The best kernel configuration and work decomposition for these sizes; with
 // allow_ws false only plans that need no workspace are considered, otherwise
-// only plans whose workspace is at most ws_cap bytes.
+// only plans whose workspace is at most ws_cap bytes.  wave_ok: the operands
+// allow the wave-independent kernel's 16-byte loads (configuration 5).
 Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int64_t CL,
-                 bool allow_ws, bool conv = false, size_t ws_cap = SIZE_MAX) {
+                 bool allow_ws, bool conv = false, size_t ws_cap = SIZE_MAX,
+                 bool wave_ok = true) {
     Choice best;
     const int cus = device_cus();
     if (cus <= 0) return best;
@@ -317,7 +332,9 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
             if (mf) {
                 const MfmaShape sh = mfma_shape(cfg);
                 if (CL % sh.kstep != 0) continue;
-                if (cfg >= 3 && CL != 64) continue;     // 64-product chunks only
+                if ((cfg == 3 || cfg == 4) && CL != 64) continue;   // 64-product chunks only
+                if (cfg == 5 && (!wave_ok || (!tb && (!allow_ws || wave_bt_bytes(N, K) > ws_cap))))
+                    continue;
                 fn = mfma_kernel(cfg, ta, tb);
                 NT = sh.NT, BM = sh.BM, BN = sh.BN;
                 t_out = mfma_cost_per_output_chunk(cfg, CL);
@@ -360,7 +377,17 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                 // chunk-per-wave and chain kernels have no shared tiles
                 if (split && mf && cfg >= 2) continue;
                 if (split && !mf && is_chain(cfg)) continue;
-                if (!split) {
+                if (!split && mf && cfg == 5) {
+                    // one tile per workgroup (the hardware deals the next
+                    // workgroup to whichever CU has room: measured a few %
+                    // faster than a persistent grid on the conv stage)
+                    const int64_t G = force_g > 0 && force_g < T ? force_g : T;
+                    p.G = (int)G;
+                    p.t_whole = T;
+                    p.L = 0;
+                    est = (double)T / cus * (nch * t_chunk + t_tile) +
+                          (tb ? 0.0 : wave_bt_cost(N, K));
+                } else if (!split) {
                     const int64_t G = T < gmax ? T : gmax;
                     p.G = (int)G;
                     p.t_whole = T;
@@ -411,11 +438,15 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                     best.BN = BN;
                     best.plan = p;
                     best.ws_bytes = ws;
+                    best.bt_bytes = mf && cfg == 5 && !tb ? wave_bt_bytes(N, K) : 0;
                     best.est_s = est;
                 }
             }
         }
     }
+    if (verbose)
+        fprintf(stderr, "[fp8t plan] chose kind %d cfg %d G %d t_whole %lld L %lld\n", (int)kind,
+                best.cfg, best.plan.G, (long long)best.plan.t_whole, (long long)best.plan.L);
     return best;
 }
 
@@ -498,8 +529,10 @@ Kind kind_of(int mode, int64_t K, int64_t CL) {
 // Workspace of a plan: the chunk sums of its shared tiles, and (entry points
 // with an FP8 result) room for their first pieces' running sums.
 size_t plan_workspace(const Choice& ch, bool fp8out) {
-    if (ch.cfg < 0 || ch.plan.L == 0) return 0;
-    size_t b = ch.ws_bytes;
+    if (ch.cfg < 0) return 0;
+    size_t b = ch.bt_bytes;
+    if (ch.plan.L == 0) return b;
+    b += ch.ws_bytes;
     if (fp8out)
         b += (size_t)(ch.plan.L / ch.plan.nch) * ch.BM * ch.BN * sizeof(uint16_t) + kWsAlign;
     return b;
@@ -546,10 +579,16 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     }
     // With no workspace, the best plan that needs none; with one, the best
     // plan overall, which must then fit; with the scratch, the best plan that
-    // fits in it.
+    // fits in it.  Operands that rule out the wave-independent kernel's
+    // 16-byte loads (which the workspace query assumes) also take the best
+    // plan that fits.
+    // (and keep a block's 32 rows within 32-bit byte offsets)
+    const bool wave_ok = !p16 && aligned(A, 16) && lda % 16 == 0 && lda < (1 << 26) &&
+                         (trans_b ? aligned(B, 16) && ldb % 16 == 0 && ldb < (1 << 26)
+                                  : K < (1 << 26));
     const Kind kind = p16 ? VALU_P16 : kind_of(mode, K, cl);
     const Choice ch = plan_gemm(kind, trans_a, trans_b, M, N, K, cl, workspace_bytes > 0, false,
-                                use_scratch ? workspace_bytes : SIZE_MAX);
+                                use_scratch || !wave_ok ? workspace_bytes : SIZE_MAX, wave_ok);
     if (ch.cfg < 0) return FP8T_EHIP;
     if (plan_workspace(ch, fp8out) > workspace_bytes) return FP8T_EWORKSPACE;
     GemmArgs g{};
@@ -588,6 +627,18 @@ int gemm_call(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, int64_t
     g.c8_vec4 = C8 && aligned(C8, 4) && ldc8 % 4 == 0;
     // FP8T_GEMM_GUARD=0 runs every piece on the safe path (tests, tuning).
     g.guarded = env_int("FP8T_GEMM_GUARD", 1) != 0;
+    if (ch.bt_bytes > 0) {
+        // the wave-independent kernel reads B k-contiguous: its copy, at the
+        // start of the workspace (the plan has no shared tiles)
+        const uintptr_t base = ((uintptr_t)workspace + kWsAlignBt - 1) & ~(uintptr_t)(kWsAlignBt - 1);
+        uint8_t* bt = reinterpret_cast<uint8_t*>(base);
+        const int64_t ldt = (K + 15) / 16 * 16;
+        launch_transpose_bytes(B, ldb, k, n, bt, ldt, stream);
+        g.B = bt;
+        g.ldb = ldt;
+        g.b_vec = 1;
+        g.b_vec16 = 1;
+    }
     return launch_plan(ch, g, stream);
 }
 }  // namespace

@@ -32,7 +32,7 @@ struct MfmaShape {
     int BK;         // k per LDS slab
 };
 
-constexpr int kMfmaConfigs = 5;
+constexpr int kMfmaConfigs = 6;
 
 MfmaShape mfma_shape(int cfg);
 
@@ -56,5 +56,17 @@ const void* mfma_kx_kernel_aligned(int ta, int tb);
 // only; its aligned variant under the same conditions.
 const void* mfma_kx16_kernel(int ta, int tb);
 const void* mfma_kx16_kernel_aligned(int ta, int tb);
+
+// 32 x 128 tiles, each of the 4 waves streaming its own 32 x 32 block with
+// no workgroup barrier (gemm_mfma_wave.hip), configuration 5: CL a multiple
+// of 64, whole tiles only, A k-contiguous (trans_a = 0) and 16-byte loads of
+// A and of a k-contiguous B (B itself when trans_b = 1, else the copy
+// launch_transpose_bytes makes), leading dimensions below 2^26; nullptr for
+// trans_a = 1.
+const void* mfma_wave_kernel(int ta);
+// Bt[n * ldt + k] = B[k * ldb + n] for k < K, n < N, on `stream` (Bt 16-byte
+// aligned, ldt a multiple of 16).
+void launch_transpose_bytes(const uint8_t* B, int64_t ldb, int K, int N, uint8_t* Bt, int64_t ldt,
+                            hipStream_t stream);
 
 }  // namespace fp8t

@@ -496,6 +496,7 @@ MfmaShape mfma_shape(int cfg) {
         case 2: return MfmaShape{32, 64, 64, kNT, 64, 64};      // CL a multiple of 64
         case 3: return MfmaShape{32, 64, 64, 1024, 64, 256};    // CL = 64, 16 waves
         case 4: return MfmaShape{16, 64, 64, 1024, 64, 256};    // CL = 64, 16 waves
+        case 5: return MfmaShape{32, 32, 128, kNT, 64, 128};   // CL a multiple of 64, 4 waves
         default: return MfmaShape{16, 32, 32, kNT, 32, 128};
     }
 }
@@ -507,6 +508,7 @@ const void* mfma_kernel(int cfg, int ta, int tb) {
         case 2: return mfma_stream_kernel(ta, tb);
         case 3: return mfma_kx_kernel(ta, tb);
         case 4: return mfma_kx16_kernel(ta, tb);
+        case 5: return (void)tb, mfma_wave_kernel(ta);
         default: return nullptr;
     }
 }

@@ -350,7 +350,8 @@ void chunk_gemm_mfma_stream(GemmArgs g, Plan p) {
     struct Pos {
         Item it;
         int ks;
-        bool ok;
+        int ok;                    // an int: a copy of Pos has no padding bytes (which
+                                   // went through scratch memory with a bool here)
     };
     Pos cur;
     cur.ok = g.guarded && work.next(p, g, cur.it);

@@ -309,7 +309,7 @@ def test_chunk_gemm_workspace_contract():
         assert np.array_equal(host(C), Co)
 
 
-@pytest.mark.parametrize("mtile", ["auto", "0", "1", "2", "3", "4"])
+@pytest.mark.parametrize("mtile", ["auto", "0", "1", "2", "3", "4", "5"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_chunk_gemm_fast_within_tolerance(ta, tb, mtile, monkeypatch):
     """Fast mode against the fast oracle within the derived tolerance, for
@@ -389,7 +389,7 @@ def test_chunk_gemm_fast_shared_tiles(mtile, wgs, ta, tb, monkeypatch):
 
 
 @pytest.mark.parametrize("mtile,split", [("0", "0"), ("1", "0"), ("2", "0"), ("3", "0"),
-                                         ("4", "0"), ("0", "1"), ("1", "1")])
+                                         ("4", "0"), ("5", "0"), ("0", "1"), ("1", "1")])
 def test_chunk_gemm_fast_specials(mtile, split, monkeypatch):
     """Inf and NaN operands through every matrix-core kernel, in whole tiles
     and in the later pieces of shared tiles (chunk sums through the
@@ -550,6 +550,89 @@ def test_chunk_gemm_fast_block_per_wave_same_bits(ta, tb, monkeypatch):
             check_fast(got["40", "1"], A, B, 64, ta, tb, f"fast kx16 {M}x{N}x{K}", Co=Co,
                        absum=abs_dot(va, vb), K=K)
 
+
+
+@pytest.mark.parametrize("tb", [0, 1])
+def test_chunk_gemm_fast_wave_kernel_same_bits(tb, monkeypatch, capfd):
+    """The wave-independent 32 x 128-tile kernel (each wave streams its own
+    32 x 32 block; loads of whole 128-byte row pieces re-laid out through
+    wave-private LDS; B stored with n contiguous copied k-contiguous first)
+    issues the streamed kernel's matrix-core instructions with the same lane
+    layout and the same epilogue, so the two give the same bits: ragged M, N
+    and K (K not a multiple of 16 or 64), padded leading dimensions, CL 64 and
+    128, one and several tiles per workgroup, both epilogues, Inf/NaN
+    operands and tiles failing the overflow guard, the FP8 result in the same
+    pass; within the fast oracle's bounds.  Operands that rule out its
+    16-byte loads fall back to another plan with the same bits."""
+    rng = np.random.default_rng(640 + tb)
+    cases = [(32, 128, 128, 64, 0), (33, 31, 65, 64, 0), (100, 70, 64 * 9 + 17, 64, 0),
+             (64, 200, 64 * 14, 128, 0), (70, 45, 64 * 23 + 40, 64, 16),
+             (40, 72, 64 * 6 + 5, 128, 32), (128, 256, 1024, 64, 0), (96, 384, 512, 64, 0)]
+    for ci, (M, N, K, CL, pad) in enumerate(cases):
+        A, B = _operands(rng, M, N, K, 0, tb)
+        if ci == len(cases) - 1:
+            A[37, :] = 0x7B                                     # 57344
+            (B if tb else B.T)[70, :] = np.where(rng.random(K) < 0.5, 0x7A, 0xFA)
+        if ci == 4:
+            A[3, 70] = 0x7C                                     # +Inf
+            (B if tb else B.T)[9, 1000] = 0x7D                  # NaN
+        # leading dimensions that keep 16-byte loads (the kernel's condition)
+        lda = -(-A.shape[1] // 16) * 16 + pad
+        ldb = (-(-B.shape[1] // 16) * 16 if tb else B.shape[1]) + pad
+        Ap = np.zeros((A.shape[0], lda), np.uint8)
+        Bp = np.zeros((B.shape[0], ldb), np.uint8)
+        Ap[:, :A.shape[1]] = A
+        Bp[:, :B.shape[1]] = B
+        Ad, Bd = dev(Ap), dev(Bp)
+        got = {}
+        for mtile, wgs in (("2", "0"), ("5", "0"), ("5", "3")):
+            monkeypatch.setenv("FP8T_MFMA_TILE", mtile)
+            monkeypatch.setenv("FP8T_GEMM_WGS", wgs)     # 3: several tiles per workgroup
+            for guard in ("1", "0"):
+                monkeypatch.setenv("FP8T_GEMM_GUARD", guard)
+                monkeypatch.setenv("FP8T_GEMM_VERBOSE", "1")
+                say(f"fast wave kernel mtile={mtile} wgs={wgs} guard={guard} tb={tb} "
+                    f"{M}x{N}x{K} CL={CL} pad={pad}")
+                capfd.readouterr()
+                got[mtile + wgs, guard] = host(gemm(Ad, Bd, M, N, K, CL, 0, tb,
+                                                    mode=fp8t.FAST, lda=lda, ldb=ldb))
+                monkeypatch.delenv("FP8T_GEMM_VERBOSE")
+                # the forced configuration is the one that ran
+                assert f"chose kind 2 cfg {mtile} " in capfd.readouterr().err
+        monkeypatch.delenv("FP8T_GEMM_WGS")
+        ref = got["20", "1"]
+        for key, C in got.items():
+            assert np.array_equal(C, ref), (key, M, N, K, np.argwhere(C != ref)[:5])
+        monkeypatch.setenv("FP8T_GEMM_GUARD", "1")
+        monkeypatch.setenv("FP8T_MFMA_TILE", "5")
+        for with_c in (True, False):
+            C8 = torch.full((M, N + 3), 0xEE, dtype=torch.uint8, device=DEV)
+            C = torch.empty((M, N), dtype=torch.uint16, device=DEV) if with_c else None
+            ws_b = fp8t.chunk_gemm_fp8_workspace_size(0, tb, M, N, K, CL, fp8t.FAST)
+            ws = torch.empty(max(ws_b, 1), dtype=torch.uint8, device=DEV)
+            fp8t.chunk_gemm_fp8(0, tb, M, N, K, CL, Ad, lda, Bd, ldb, C, N, C8, N + 3,
+                                0.5, fp8t.FAST, ws, ws_b)
+            q8 = host(C8)
+            assert np.all(q8[:, N:] == 0xEE)
+            assert np.array_equal(q8[:, :N], oracle.fp8_quantize(ref, 0.5))
+            if with_c:
+                assert np.array_equal(host(C), ref)
+        # a misaligned A base rules the kernel out: another plan, same bits
+        Am = torch.zeros(Ap.size + 1, dtype=torch.uint8, device=DEV)
+        Am[1:] = Ad.reshape(-1)
+        C = torch.empty((M, N), dtype=torch.uint16, device=DEV)
+        ws_b = fp8t.chunk_gemm_workspace_size(0, tb, M, N, K, CL, fp8t.FAST)
+        ws = torch.empty(max(ws_b, 1), dtype=torch.uint8, device=DEV)
+        say(f"fast wave kernel misaligned A tb={tb} {M}x{N}x{K}")
+        fp8t.chunk_gemm(0, tb, M, N, K, CL, Am.data_ptr() + 1, lda, Bd, ldb, C, N, fp8t.FAST,
+                        ws, ws_b)
+        assert np.array_equal(host(C), ref)
+        if ci != 4:
+            Co = oracle.chunk_gemm(A, B, CL, 0, tb, mode=oracle.FAST)
+            va = oracle.p8_value(A)
+            vb = oracle.p8_value(B.T if tb else B)
+            check_fast(got["50", "1"], A, B, CL, 0, tb, f"fast wave {M}x{N}x{K}", Co=Co,
+                       absum=abs_dot(va, vb), K=K)
 
 def test_chunk_gemm_padded_leading_dims_and_misaligned_bases():
     rng = np.random.default_rng(530)
