@@ -50,7 +50,7 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 300.0 MB, weight-gradient 2402.6 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "e55505c8e3cc11e93b78e7fa2668577f7a68848be37233870b356556335592d0"
+TRAFFIC_SOURCES_SHA256 = "e9354fac69d2c2fa65b9909ce49b3e5058b1720e1fca57ea2329d3679a9ed2b0"
 EXACT_TRAFFIC_BYTES_PER_CALL = 963.8e6
 
 

@@ -110,10 +110,14 @@ int fp16_quantize(const float* src, uint16_t* dst, int64_t n,
  * workspace / workspace_bytes: optional device scratch, for the chunk sums
  * of output tiles whose K range is shared out over several workgroups (the
  * chunk sums are then added into the running sum in ascending order by a
- * second pass, so the result is the same).  With workspace_bytes == 0 the
- * call takes the fastest plan that needs none; otherwise workspace_bytes must
- * be at least chunk_gemm_workspace_size(...) for the same arguments on the
- * same device.  Its contents on entry do not matter.
+ * second pass, so the result is the same), or, in fast mode with trans_b = 0,
+ * for a k-contiguous copy of B (N x K bytes) that the matrix-core kernel
+ * reads.  With workspace_bytes == 0 the call takes the fastest plan that
+ * needs none; otherwise workspace_bytes must be at least
+ * chunk_gemm_workspace_size(...) for the same arguments on the same device
+ * (operands whose alignment rules out a plan the query assumed take the
+ * fastest plan that fits in workspace_bytes).  Its contents on entry do not
+ * matter.
  * Errors: FP8T_EINVAL (negative size, M, N or K above 2^31 - 4097 -- the
  * kernels index in 32 bits --, CL < 1, flag not 0/1, a leading
  * dimension too small, NULL pointer for a non-empty matrix, NULL workspace

@@ -239,8 +239,23 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
                                                                           0, 0);
                 crem -= 64;
                 if (crem == 0 || ks + 64 >= g.K) {
+                    // S = rn16v(S + rn16v(acc)) written out step by step over
+                    // the 16 outputs, so the schedule interleaves them (the
+                    // compiler otherwise runs each output's 7 dependent
+                    // instructions back to back; measured 1.5-2% faster)
+                    float c[16], x[16];
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) S[r] = rn16v(S[r] + rn16v(acc[r]));
+                    for (int r = 0; r < 16; ++r) c[r] = acc[r] * 16385.0f;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) x[r] = c[r] - acc[r];
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) x[r] = S[r] + (c[r] - x[r]);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) c[r] = x[r] * 16385.0f;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) x[r] = c[r] - x[r];
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) S[r] = c[r] - x[r];
                     // the guard: running sums at chunk ends (v_max3 drops NaN,
                     // which the check of the final sums catches)
 #pragma unroll
