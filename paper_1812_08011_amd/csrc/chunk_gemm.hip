@@ -385,7 +385,11 @@ Choice plan_gemm(Kind kind, int ta, int tb, int64_t M, int64_t N, int64_t K, int
                     p.G = (int)G;
                     p.t_whole = T;
                     p.L = 0;
-                    est = (double)T / cus * (nch * t_chunk + t_tile) +
+                    // fewer tiles than CUs: a lone tile is not done faster
+                    // than 2.3 tiles' CU time (its waves wait on their own
+                    // latency; measured on 64 tiles of K 6000)
+                    const double per_cu = (double)T / cus;
+                    est = (T < cus ? 2.3 : per_cu) * (nch * t_chunk + t_tile) +
                           (tb ? 0.0 : wave_bt_cost(N, K));
                 } else if (!split) {
                     const int64_t G = T < gmax ? T : gmax;

@@ -43,10 +43,13 @@ def _operands(rng, M, N, K, ta, tb):
     return A, B
 
 
-# (M, N, K, CL, ta, tb, env): shared tiles through the scratch, then a smaller
-# call, then a call whose fastest plan needs more than the scratch
+# (M, N, K, CL, ta, tb, env): shared tiles through the scratch, then smaller
+# calls, then a call whose fastest plan needs more than the scratch
 CASES = [
     (512, 384, 8192, 64, 0, 0, {"FP8T_GEMM_SPLIT": "1"}),
+    # fast mode: the matrix-core kernel that reads a k-contiguous copy of B
+    # (made in the scratch)
+    (300, 640, 2048, 64, 0, 0, {"FP8T_MFMA_TILE": "5"}),
     (200, 150, 3000, 64, 1, 0, {"FP8T_GEMM_SPLIT": "1", "FP8T_GEMM_WGS": "7"}),
     (2304, 256, 16384, 64, 1, 0, {}),
 ]
@@ -56,7 +59,7 @@ CASES = [
 def test_noalloc_matches_chunk_gemm(mode, monkeypatch):
     rng = np.random.default_rng(1300 + mode)
     for (M, N, K, CL, ta, tb, env) in CASES:
-        for k in ("FP8T_GEMM_SPLIT", "FP8T_GEMM_WGS"):
+        for k in ("FP8T_GEMM_SPLIT", "FP8T_GEMM_WGS", "FP8T_MFMA_TILE"):
             monkeypatch.delenv(k, raising=False)
         for k, v in env.items():
             monkeypatch.setenv(k, v)
