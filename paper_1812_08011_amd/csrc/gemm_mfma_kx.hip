@@ -137,6 +137,91 @@ struct StepShare {
     }
 };
 
+// The block-per-wave kernel's share of a step (64 rows by 256 k, 16 bytes per
+// thread) and its LDS layout:
+//   KC: as StepShare (rows of k bytes, 8-byte k slots swizzled);
+//   otherwise (row index contiguous in memory): k row t / 4, row bytes
+//     16 (t % 4) .. +15, stored as they are -- LDS holds the step k-major
+//     (kTrPitch bytes per k) and the matrix-core operands are read with
+//     gfx950's transposing LDS read (ds_read_b64_tr_b8), so staging needs no
+//     byte transposes in registers.
+constexpr int kTrPitch = kT + 16;          // LDS bytes per k of a k-major step
+template <bool KC>
+struct StepShare16 {
+    static constexpr int kRows = KC ? kT : kSK;
+    static constexpr int kRowBytes = KC ? kPitch : kTrPitch;
+    uint32_t w[4];
+
+    template <bool AL>
+    __device__ __forceinline__ void load(const uint8_t* __restrict__ p, int64_t ld, int r0,
+                                         int rows, int k0, int kend, int vec, int vec16,
+                                         int tid) {
+        if (KC) {
+            const bool interior = AL || (r0 + kT <= rows && k0 + kSK <= kend);
+            const int r = r0 + (tid >> 4), k = k0 + (tid & 15) * 16;
+            if (interior && (AL || vec16)) {
+                const uint4 v = *reinterpret_cast<const uint4*>(p + (int64_t)r * ld + k);
+                w[0] = v.x, w[1] = v.y, w[2] = v.z, w[3] = v.w;
+            } else if (interior && vec) {
+                const uint32_t* q = reinterpret_cast<const uint32_t*>(p + (int64_t)r * ld + k);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) w[i] = q[i];
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) w[i] = ld4(p, ld, r, k + 4 * i, rows, kend, vec);
+            }
+        } else {
+            const int k = k0 + (tid >> 2), r = r0 + (tid & 3) * 16;
+            const bool interior = AL || (r0 + kT <= rows && k0 + kSK <= kend);
+            if (interior && (AL || vec16)) {
+                const uint4 v = *reinterpret_cast<const uint4*>(p + (int64_t)k * ld + r);
+                w[0] = v.x, w[1] = v.y, w[2] = v.z, w[3] = v.w;
+            } else if (interior && vec) {
+                const uint32_t* q = reinterpret_cast<const uint32_t*>(p + (int64_t)k * ld + r);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) w[i] = q[i];
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) w[i] = ld4(p, ld, k, r + 4 * i, kend, rows, vec);
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(uint8_t* lds, int tid) {
+        if (KC) {
+            const int r = tid >> 4, q = (tid & 15) * 2;
+            uint8_t* row = lds + r * kRowBytes;
+            *reinterpret_cast<uint2*>(row + slot_off(r, q)) = make_uint2(w[0], w[1]);
+            *reinterpret_cast<uint2*>(row + slot_off(r, q + 1)) = make_uint2(w[2], w[3]);
+        } else {
+            *reinterpret_cast<uint4*>(lds + (tid >> 2) * kRowBytes + (tid & 3) * 16) =
+                make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+
+    // The 8 operand bytes of lane l for the 16x16x32 instruction over k kb ..
+    // kb + 31: row r0 + l % 16, k kb + 8 (l / 16) .. +7.  k-major: the
+    // transposing read gives lane i of each 16-lane group, as its byte b,
+    // byte i % 8 of the 8-byte piece that lane 2 b + i / 8 of the group
+    // addresses (b = 0 .. 7; measured on gfx950), so lane l of group
+    // g = l / 16 addresses k kb + 8 g + (l % 16) / 2 at row bytes
+    // r0 + 8 (l % 2) .. +7.
+    __device__ __forceinline__ long operand(const uint8_t* lds, int r0, int kb, int lane) const {
+        if (KC) {
+            const int r = r0 + (lane & 15);
+            const int q = kb / 8 + (lane >> 4);
+            return *reinterpret_cast<const long*>(lds + r * kRowBytes + slot_off(r, q));
+        } else {
+            typedef int v2i __attribute__((ext_vector_type(2)));
+            const int s = lane & 15;
+            const uint8_t* a = lds + (kb + 8 * (lane >> 4) + (s >> 1)) * kRowBytes + r0 + 8 * (s & 1);
+            const v2i v = __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                (__attribute__((address_space(3))) v2i*)(a));
+            return (long)(uint32_t)v.x | ((long)(uint32_t)v.y << 32);
+        }
+    }
+};
+
 // Result register r of lane l (32 x 32 block): row 8 (r / 4) + 4 (l / 32) + r % 4,
 // column l % 32; operand bytes of lane l: row (or column) l % 32.
 __device__ __forceinline__ int res_row(int l, int r) { return 8 * (r / 4) + 4 * (l / 32) + r % 4; }
@@ -426,8 +511,10 @@ typedef float v4f __attribute__((ext_vector_type(4)));
 template <bool TA, bool TB, bool AL>
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4)))
 void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
-    __shared__ __attribute__((aligned(16))) uint8_t As[2][kT][kPitch];
-    __shared__ __attribute__((aligned(16))) uint8_t Bs[2][kT][kPitch];
+    typedef StepShare16<!TA> ShareA;  // A is k-contiguous unless transposed
+    typedef StepShare16<TB> ShareB;   // B is k-contiguous only when transposed
+    __shared__ __attribute__((aligned(16))) uint8_t As[2][ShareA::kRows * ShareA::kRowBytes];
+    __shared__ __attribute__((aligned(16))) uint8_t Bs[2][ShareB::kRows * ShareB::kRowBytes];
     __shared__ __attribute__((aligned(16))) uint16_t Os[kT * kT];
     __shared__ int redo[kRedoMax];
     __shared__ int n_redo;
@@ -439,7 +526,6 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
     // row (column) l % 16, k bytes 8 (l / 16) .. +7 of each 32-k instruction,
     // and results at rows 4 (l / 16) + r, column l % 16 of the block
     const int bi = wave >> 2, bj = wave & 3;
-    const int arow = 16 * bi + (lane & 15), bcol = 16 * bj + (lane & 15);
     const int kg = lane >> 4;
     const int orow = 16 * bi + 4 * kg, ocol = 16 * bj + (lane & 15);
     if (tid == 0) {
@@ -448,8 +534,8 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
     }
     int vslot = 0;
 
-    StepShare<!TA> sa;             // A is k-contiguous unless transposed
-    StepShare<TB> sb;              // B is k-contiguous only when transposed
+    ShareA sa;
+    ShareB sb;
     float S[4];
     float vmax = 0.0f;
     const v4f zero = {};
@@ -479,9 +565,9 @@ void chunk_gemm_mfma_kx16(GemmArgs g, Plan p) {
             if (!AL && s * kWaves + c >= nch) continue;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const int q = (kCL * c + 32 * h) / 8 + kg;       // 8-byte k slot
-                const long av = *reinterpret_cast<const long*>(&As[buf][arow][slot_off(arow, q)]);
-                const long bv = *reinterpret_cast<const long*>(&Bs[buf][bcol][slot_off(bcol, q)]);
+                const int kb = kCL * c + 32 * h;
+                const long av = sa.operand(As[buf], 16 * bi, kb, lane);
+                const long bv = sb.operand(Bs[buf], 16 * bj, kb, lane);
                 acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf8_bf8(av, bv, acc[c], 0, 0, 0);
             }
         }
