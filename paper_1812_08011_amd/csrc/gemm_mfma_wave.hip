@@ -46,6 +46,14 @@ constexpr int kRedoMax = 32;               // failed tiles remembered per wave
 // Result register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
 __device__ __forceinline__ int out_row(int l, int r) { return 8 * (r / 4) + 4 * (l / 32) + r % 4; }
 
+// max(m, |a|, |b|) with NaN propagating (IEEE 754-2019 maximum): any NaN
+// operand gives NaN.
+__device__ __forceinline__ float maximum3_abs(float m, float a, float b) {
+    float r;
+    asm("v_maximum3_f32 %0, %1, |%2|, |%3|" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+    return r;
+}
+
 // Orders a wave's LDS accesses across its lanes: the LDS executes one wave's
 // instructions in order, and the fences keep the compiler from moving
 // accesses across.
@@ -256,21 +264,21 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
                     for (int r = 0; r < 16; ++r) x[r] = c[r] - x[r];
 #pragma unroll
                     for (int r = 0; r < 16; ++r) S[r] = c[r] - x[r];
-                    // the guard: running sums at chunk ends (v_max3 drops NaN,
-                    // which the check of the final sums catches)
+                    // the guard: running sums at chunk ends, with gfx950's
+                    // NaN-propagating three-input maximum (a NaN sum, from an
+                    // Inf/NaN operand, stays NaN to the block end and so
+                    // fails the check there without a test of each sum)
 #pragma unroll
-                    for (int r = 0; r < 16; r += 2) vmax = max3_abs(vmax, S[r], S[r + 1]);
+                    for (int r = 0; r < 16; r += 2) vmax = maximum3_abs(vmax, S[r], S[r + 1]);
                     crem = g.CL;
                 }
             }
             wave_lds_sync();
             if (k + kRound >= g.K) {
                 // block end: running sums below 2^31 at every chunk end -- no
-                // chunk sum or sum reached FP16's overflow threshold; no
-                // Inf/NaN operand (its NaN stays in the running sum)
-                bool bad = !(vmax < 2147483648.0f);
-#pragma unroll
-                for (int r = 0; r < 16; ++r) bad |= !(fabsf(S[r]) < 2147483648.0f);
+                // chunk sum or sum reached FP16's overflow threshold -- and
+                // never NaN (no Inf/NaN operand)
+                const bool bad = !(vmax < 2147483648.0f);
                 if (__any(bad)) {
                     if (nred < kRedoMax && lane == 0) redo[wave][nred] = ordinal;
                     ++nred;
