@@ -109,18 +109,19 @@ __device__ __forceinline__ uint16_t f32d_to_fp16(float x) {
 // FP16 code of a plain value that is already on the FP16 grid and below
 // 2^32 in magnitude -- what the exact mode's guarded path holds; a piece in
 // which a value left that range fails the guard and is recomputed on the
-// safe path, which overwrites whatever this wrote.  Normal values (from
-// 2^-30) by moving the fields, subnormal ones (m 2^-39) by scaling m back to
-// an integer: the same codes as f32d_to_fp16<0> in that range, without its
-// Inf/NaN/overflow cases.  The code comes in the low 16 bits of a 32-bit
-// word whose upper bits are zero in that range (callers pack two codes
+// safe path, which overwrites whatever this wrote.  x 2^-96 is exact in
+// FP32 (FP32's exponent bias exceeds FP16's by 96): for normal FP16 values
+// (from 2^-30) its exponent field is the FP16 one (1 .. 62 below 2^32) and
+// its top 9 significand bits the FP16 ones; for subnormal ones (m 2^-39) it
+// is the FP32 subnormal m 2^14 2^-149 (denormals are kept).  Either way its
+// bits 14 .. 28 are the code's exponent and significand and bit 31 its sign:
+// the same codes as f32d_to_fp16<0> in that range, without its
+// Inf/NaN/overflow cases, in 4 instructions.  The code comes in the low 16
+// bits of a 32-bit word whose upper bits are zero (callers pack two codes
 // without masking).
 __device__ __forceinline__ uint32_t f32g_to_fp16(float x) {
-    const uint32_t u = __float_as_uint(x);
-    const uint32_t a = u & 0x7FFFFFFFu;
-    const uint32_t n = (a >> 14) - (96u << 9);
-    const uint32_t k = (uint32_t)(__uint_as_float(a) * 0x1p39f);
-    return ((u >> 16) & 0x8000u) | (a >= (97u << 23) ? n : k);
+    const uint32_t b = __float_as_uint(x * 0x1p-96f);
+    return ((b >> 14) & 0x7FFFu) | ((b >> 16) & 0xFFFF8000u);
 }
 
 // FP16 code of a GEMM result in the domain scaled by 2^DOM: 0 is the

@@ -159,20 +159,20 @@ def test_fp16_product_magic_rounding_scaled():
 
 
 def test_guarded_fp16_encode_round_trips_every_code():
-    """The exact kernel's guarded-path encoder (fields moved for values from
-    2^-30, subnormals m 2^-39 scaled back to m): every finite FP16 code below
-    2^32, both signs, decoded by the oracle's definition and encoded with
-    float32 arithmetic, gives the code back (-0 included)."""
+    """The guarded paths' encoder (x 2^-96 in float32 -- an FP32 subnormal
+    for FP16 subnormals --, its bits 14-28 as exponent and significand, bit
+    31 as sign): every finite FP16 code below 2^32, both signs, decoded by
+    the oracle's definition and encoded with float32 arithmetic that keeps
+    subnormals, gives the code back (-0 included), with zero upper bits."""
     import oracle
     codes = np.arange(1 << 16, dtype=np.uint32)
     finite = (codes & 0x7E00) != 0x7E00
     codes = codes[finite]
     x = oracle.p16_value(codes.astype(np.uint16)).astype(np.float32)
-    u = x.view(np.uint32)
-    a = u & np.uint32(0x7FFFFFFF)
-    n = (a >> np.uint32(14)) - np.uint32(96 << 9)
-    normal = a >= np.uint32(97 << 23)
-    k = np.zeros_like(a)
-    k[~normal] = (a[~normal].view(np.float32) * np.float32(2.0 ** 39)).astype(np.uint32)
-    enc = ((u >> np.uint32(16)) & np.uint32(0x8000)) | np.where(normal, n, k)
+    assert np.all(np.abs(x) < np.float32(2.0 ** 32))
+    y = x * np.float32(2.0 ** -96)
+    # the scaling is exact (the FP32 subnormal range included)
+    assert np.array_equal(y.astype(np.float64) * 2.0 ** 96, x.astype(np.float64))
+    b = y.view(np.uint32)
+    enc = ((b >> np.uint32(14)) & np.uint32(0x7FFF)) | ((b >> np.uint32(16)) & np.uint32(0xFFFF8000))
     assert np.array_equal(enc, codes)
