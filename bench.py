@@ -50,8 +50,8 @@ FP8_MFMA_MAC_S = 5.0e15 / 2                             # dense FP8 5.0 PFLOP/s
 # backward-data 300.0 MB, weight-gradient 2402.6 MB including the chunk sums
 # of its shared tiles and the fold pass).  Valid only for the kernel sources
 # they were measured on (EXACT_KERNEL_SOURCES): any change to them reports null.
-TRAFFIC_SOURCES_SHA256 = "a9b88b9223183d6ec26581684ad10291aeb54c2f4593ef0f1e824ace12a92b60"
-EXACT_TRAFFIC_BYTES_PER_CALL = 963.9e6
+TRAFFIC_SOURCES_SHA256 = "db50901dabab05030d5d7fa646f332cc0669e2180f3c2ded13dbd31be5b5c982"
+EXACT_TRAFFIC_BYTES_PER_CALL = 963.8e6
 
 
 # The sources that decide what an exact-mode chunk_gemm call runs: the VALU
