@@ -15,13 +15,19 @@
 //     bytes, so each load instruction touches 8 whole 128-byte lines (the
 //     matrix-core layout, 32 bytes of 32 rows per lane group, would touch
 //     32 lines per instruction, and loads in that layout measured 2x slower);
-//   * the round goes through a wave-private LDS tile into the matrix-core
-//     layout, while the next round (of the same tile or the wave's next
-//     one) is already in flight into registers;
+//   * the round goes straight from memory into a wave-private LDS tile
+//     (gfx950's global_load_lds_dwordx4: lane l of a load lands at its LDS
+//     base + 16 l, so which 16 bytes a lane fetches sets the layout: the
+//     pieces of a row are XOR-swizzled by the row, which keeps the
+//     matrix-core reads free of bank conflicts); the wave reads both slabs'
+//     operands from it into registers and then already starts the next
+//     round (of the same tile or its next one) into it, so the loads bypass
+//     the registers and take no LDS write instructions;
 //   * the guard is per wave (its outputs depend on no other wave's): a tile
-//     whose running sums reached 2^31 at a chunk end or ended NaN is listed
-//     and recomputed after the stream with the 2^96-scaled epilogue;
-//   * the finished block's FP16 codes leave through the same LDS tile as
+//     whose running sums reached 2^31 at a chunk end or ended NaN is marked
+//     (one bit per tile ordinal) and recomputed after the stream with the
+//     2^96-scaled epilogue;
+//   * the finished block's FP16 codes leave through a second LDS tile as
 //     16-byte row pieces.
 // Rows of A beyond M and of B beyond N are read as row M-1 / N-1 (their
 // outputs are not stored); k beyond K reads as zero.
@@ -39,12 +45,15 @@ constexpr int kWaves = 4;                  // waves per workgroup
 constexpr int kNT = 64 * kWaves;
 constexpr int kBM = 32, kBN = 32 * kWaves; // workgroup tile; a wave's block is 32 x 32
 constexpr int kRound = 128;                // k per load round: two 64-k slabs
-constexpr int kP = kRound + 16;            // LDS row pitch (bytes) of a round
+constexpr int kP = kRound;                 // LDS row pitch (bytes) of a round
 constexpr int kOP = 64;                    // LDS row pitch (bytes) of the staged codes
-constexpr int kRedoMax = 32;               // failed tiles remembered per wave
 
 // Result register r of lane l: row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
 __device__ __forceinline__ int out_row(int l, int r) { return 8 * (r / 4) + 4 * (l / 32) + r % 4; }
+// LDS byte offset of 16-byte segment g of row r of a round (segments XOR-swizzled by r % 8)
+__device__ __forceinline__ int seg_off(int r, int g) { return r * kP + 16 * (g ^ (r & 7)); }
+typedef __attribute__((address_space(1))) const void* gptr_t;
+typedef __attribute__((address_space(3))) void* lptr_t;
 
 // max(m, |a|, |b|) with NaN propagating (IEEE 754-2019 maximum): any NaN
 // operand gives NaN.
@@ -79,14 +88,18 @@ __device__ __forceinline__ vu4 load16(const uint8_t* __restrict__ p, int64_t ld,
 __global__ __launch_bounds__(kNT) __attribute__((amdgpu_waves_per_eu(4)))
 void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
     __shared__ __attribute__((aligned(16))) uint8_t lds[kWaves][2][kBM * kP];
-    __shared__ int redo[kWaves][kRedoMax];
+    __shared__ __attribute__((aligned(16))) uint8_t lco_all[kWaves][kBM * kOP];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     uint8_t* const la = lds[wave][0];
     uint8_t* const lb = lds[wave][1];
+    uint8_t* const lco = lco_all[wave];
     const int rl = lane & 31, kh = 32 * (lane >> 5);   // operand row, k half
-    const int lr = lane >> 3, lc = 16 * (lane & 7);    // load row (of 8), byte offset
+    const int lr = lane >> 3;                          // load row (of 8)
+    // the global 16-byte segment a lane loads: its LDS slot (lane % 8) XOR
+    // the row's swizzle (row % 8 = lane / 8)
+    const int lc = 16 * ((lane & 7) ^ lr);
     const v16f zero = {};
 
     auto geom = [&](int64_t t, int& m0, int& n0) __attribute__((always_inline)) {
@@ -97,20 +110,20 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
     };
 
     // The FP16 codes of the wave's block (running sums S, DOM their value
-    // scale) to C and / or the FP8 result C8, through the LDS tile la.
+    // scale) to C and / or the FP8 result C8, through the LDS tile lco.
     auto store_block = [&](auto dom_tag, const float (&S)[16], int m0, int n0)
                            __attribute__((always_inline)) {
         constexpr int DOM = decltype(dom_tag)::value;
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-            *reinterpret_cast<uint16_t*>(la + out_row(lane, r) * kOP + 2 * rl) =
+            *reinterpret_cast<uint16_t*>(lco + out_row(lane, r) * kOP + 2 * rl) =
                 (uint16_t)fp16_code<DOM>(S[r]);
         wave_lds_sync();
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
             const int u = lane + 64 * q;
             const int row = u >> 2, col = (u & 3) * 8;
-            const vu4 v = *reinterpret_cast<const vu4*>(la + row * kOP + 2 * col);
+            const vu4 v = *reinterpret_cast<const vu4*>(lco + row * kOP + 2 * col);
             const int m = m0 + row, n = n0 + col;
             if (m >= g.M || n >= g.N) continue;
             if (g.C) {
@@ -140,7 +153,7 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
                 }
             }
         }
-        wave_lds_sync();                 // la is rewritten by the next round
+        wave_lds_sync();                 // lco is rewritten at the next block end
     };
 
     // ---- the stream (guarded epilogue) ----
@@ -162,27 +175,33 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
             ob[q] = (uint32_t)((min(n0 + 8 * q + lr, g.N - 1) - nb) * (int)g.ldb + lc);
         }
     };
-    vu4 ra[4], rb[4];
-    // loads of the round at k of the block whose rows() were taken last
+    // the round at k of the block whose rows() were taken last, into the
+    // LDS tiles: whole rounds straight from memory (lane l of load q lands at
+    // q KB + 16 l: row 8 q + l / 8, slot l % 8), a last partial round through
+    // registers with the bytes past K zeroed
     auto issue = [&](int k) __attribute__((always_inline)) {
         const uint8_t* const ak = pa + k;
         const uint8_t* const bk = pb + k;
         if (k + kRound <= g.K) {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                ra[q] = *reinterpret_cast<const vu4*>(ak + oa[q]);
-                rb[q] = *reinterpret_cast<const vu4*>(bk + ob[q]);
+                __builtin_amdgcn_global_load_lds((gptr_t)(ak + oa[q]), (lptr_t)(la + q * 1024), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((gptr_t)(bk + ob[q]), (lptr_t)(lb + q * 1024), 16, 0, 0);
             }
         } else {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                ra[q] = load16(pa, 0, 0, (int)oa[q] + k, (int)(oa[q] - lc) + g.K);
-                rb[q] = load16(pb, 0, 0, (int)ob[q] + k, (int)(ob[q] - lc) + g.K);
+                const vu4 va = load16(pa, 0, 0, (int)oa[q] + k, (int)(oa[q] - lc) + g.K);
+                const vu4 vb = load16(pb, 0, 0, (int)ob[q] + k, (int)(ob[q] - lc) + g.K);
+                *reinterpret_cast<vu4*>(la + q * 1024 + 16 * lane) = va;
+                *reinterpret_cast<vu4*>(lb + q * 1024 + 16 * lane) = vb;
             }
         }
     };
     // with the guarded epilogue switched off every tile takes the safe one
-    int nred = g.guarded ? 0 : kRedoMax + 1;
+    // failed blocks: ordinals below 64 as bits, any later one redoes all
+    uint64_t failed = 0;
+    bool fail_all = !g.guarded;
     int64_t t = blockIdx.x;
     if (g.guarded && t < p.t_whole) {
         int m0, n0, k = 0;
@@ -213,30 +232,35 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
         float vmax = 0.0f;             // largest |S| at chunk ends
         int crem = g.CL, ordinal = 0;
         for (;;) {
-            // this round: registers -> LDS; then the next round's loads
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                *reinterpret_cast<vu4*>(la + (8 * q + lr) * kP + lc) = ra[q];
-                *reinterpret_cast<vu4*>(lb + (8 * q + lr) * kP + lc) = rb[q];
-            }
-            if (okx) issue(kx);
+            // this round's bytes are in the LDS tiles (direct loads count in
+            // vmcnt; the compiler does not see their LDS writes)
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             wave_lds_sync();
+            v8i a8s[2], b8s[2];
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl) {
+                const int g0 = 4 * sl + kh / 16;
+                const vu4 a0 = *reinterpret_cast<const vu4*>(la + seg_off(rl, g0));
+                const vu4 a1 = *reinterpret_cast<const vu4*>(la + seg_off(rl, g0 + 1));
+                const vu4 b0 = *reinterpret_cast<const vu4*>(lb + seg_off(rl, g0));
+                const vu4 b1 = *reinterpret_cast<const vu4*>(lb + seg_off(rl, g0 + 1));
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    a8s[sl][q] = (int)a0[q];
+                    a8s[sl][4 + q] = (int)a1[q];
+                    b8s[sl][q] = (int)b0[q];
+                    b8s[sl][4 + q] = (int)b1[q];
+                }
+            }
+            // the tiles are refilled with the next round once these reads are done
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            wave_lds_sync();
+            if (okx) issue(kx);
 #pragma unroll
             for (int sl = 0; sl < 2; ++sl) {
                 const int ks = k + 64 * sl;
                 if (ks >= g.K) break;
-                v8i a8, b8;
-                const vu4 a0 = *reinterpret_cast<const vu4*>(la + rl * kP + 64 * sl + kh);
-                const vu4 a1 = *reinterpret_cast<const vu4*>(la + rl * kP + 64 * sl + kh + 16);
-                const vu4 b0 = *reinterpret_cast<const vu4*>(lb + rl * kP + 64 * sl + kh);
-                const vu4 b1 = *reinterpret_cast<const vu4*>(lb + rl * kP + 64 * sl + kh + 16);
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    a8[q] = (int)a0[q];
-                    a8[4 + q] = (int)a1[q];
-                    b8[q] = (int)b0[q];
-                    b8[4 + q] = (int)b1[q];
-                }
+                const v8i a8 = a8s[sl], b8 = b8s[sl];
                 // format selectors 1, 1: both operands bf8 (= the FP8 codes);
                 // no scaling; a chunk's first slab starts from zero
                 if (crem == g.CL)
@@ -280,8 +304,8 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
                 // never NaN (no Inf/NaN operand)
                 const bool bad = !(vmax < 2147483648.0f);
                 if (__any(bad)) {
-                    if (nred < kRedoMax && lane == 0) redo[wave][nred] = ordinal;
-                    ++nred;
+                    if (ordinal < 64) failed |= 1ull << ordinal;
+                    else fail_all = true;
                 } else {
                     store_block(std::integral_constant<int, 0>{}, S, m0, n0);
                 }
@@ -299,15 +323,12 @@ void chunk_gemm_mfma_wave(GemmArgs g, Plan p) {
     }
 
     // ---- blocks that failed the guard (all of them when it is off, or when
-    // more failed than the list holds), recomputed in the 2^96 domain ----
-    if (nred == 0) return;
-    wave_lds_sync();                     // the list entries are written
-    int ord = 0, next_listed = 0;
+    // one beyond the 64th failed), recomputed in the 2^96 domain ----
+    if (failed == 0 && !fail_all) return;
+    int ord = 0;
     for (int64_t tt = blockIdx.x; tt < p.t_whole; tt += p.G, ++ord) {
-        const bool listed = nred > kRedoMax ||
-                            (next_listed < nred && redo[wave][next_listed] == ord);
+        const bool listed = fail_all || (ord < 64 && ((failed >> ord) & 1));
         if (!listed) continue;
-        if (nred <= kRedoMax) ++next_listed;
         int m0, n0;
         geom(tt, m0, n0);
         const int ar = min(m0 + rl, g.M - 1), br = min(n0 + rl, g.N - 1);
